@@ -1,0 +1,78 @@
+"""Pure-Python brute force of 3D RoPE + softmax attention, for tiny shapes.
+
+A second formulation, written independently of the oracle: the rotation of a
+channel pair is the complex product (x0 + i x1) * exp(i phi) with the token's
+coordinates found by walking the (t, h, w) grid, and the softmax is a direct
+sum of math.exp terms accumulated with math.fsum (no max subtraction, no
+matrix products).  Only usable for small sizes and moderate logits.
+"""
+
+import cmath
+import math
+
+
+def coords_by_walk(n, grid):
+    """(t, h, w) of token n found by enumerating the grid in patchify order."""
+    T, Hp, Wp = grid
+    idx = 0
+    for t in range(T):
+        for h in range(Hp):
+            for w in range(Wp):
+                if idx == n:
+                    return (t, h, w)
+                idx += 1
+    return None  # token beyond the grid: not rotated
+
+
+def rope_row(x, n, grid, dims, theta, pair_mode):
+    """Rotate one head vector x (list of floats) of token n."""
+    pos = coords_by_walk(n, grid)
+    y = list(x)
+    if pos is None:
+        return y
+    off = 0
+    for a in range(3):
+        da = dims[a]
+        half = da // 2
+        for j in range(half):
+            if pair_mode == 0:
+                c0, c1 = off + 2 * j, off + 2 * j + 1
+            else:
+                c0, c1 = off + j, off + half + j
+            phi = pos[a] * math.pow(theta, -(2.0 * j) / da)
+            z = complex(x[c0], x[c1]) * cmath.exp(1j * phi)
+            y[c0], y[c1] = z.real, z.imag
+        off += da
+    return y
+
+
+def attention(q, k, v, scale, kv_valid_len=None, rope=None):
+    """q [B][Lq][H][d], k/v [B][Lk][H][d] nested lists; rope = (grid, dims, theta, mode).
+
+    Returns (o, lse) as nested lists o[B][Lq][H][d], lse[B][H][Lq].
+    """
+    B, Lq, H, d = len(q), len(q[0]), len(q[0][0]), len(q[0][0][0])
+    Lk = len(k[0])
+    o = [[[[0.0] * d for _ in range(H)] for _ in range(Lq)] for _ in range(B)]
+    lse = [[[float("-inf")] * Lq for _ in range(H)] for _ in range(B)]
+    for b in range(B):
+        lv = Lk if kv_valid_len is None else max(0, min(Lk, int(kv_valid_len[b])))
+        for h in range(H):
+            keys = []
+            for j in range(lv):
+                kj = k[b][j][h]
+                if rope is not None:
+                    kj = rope_row(kj, j, *rope)
+                keys.append(kj)
+            for i in range(Lq):
+                qi = q[b][i][h]
+                if rope is not None:
+                    qi = rope_row(qi, i, *rope)
+                if lv == 0:
+                    continue
+                w = [math.exp(scale * math.fsum(qi[c] * keys[j][c] for c in range(d))) for j in range(lv)]
+                z = math.fsum(w)
+                for c in range(d):
+                    o[b][i][h][c] = math.fsum(w[j] * v[b][j][h][c] for j in range(lv)) / z
+                lse[b][h][i] = math.log(z)
+    return o, lse

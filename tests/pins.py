@@ -1,0 +1,257 @@
+"""Checks that pin the oracle to facts other than itself.
+
+Each check takes the functions under test as arguments so that the same checks
+run against the oracle (tests/test_oracle_pins.py) and against deliberately
+broken copies of it (tests/test_oracle_mutations.py, which shows that each
+plausible mistake is caught).  Every check raises AssertionError on failure.
+
+Sources of truth used here:
+  * closed forms of a plane rotation (unit vectors, the exact frequency
+    theta**(-1/2) = 0.01 of the middle time-pair for theta = 1e4, d_t = 44);
+  * identities the rotary embedding must satisfy (norm preservation,
+    relative-position invariance, identity at the origin, untouched tokens
+    beyond the grid);
+  * the pure-Python brute force in tests/brute.py (complex-number rotation,
+    math.fsum softmax);
+  * torch.nn.functional.scaled_dot_product_attention in float64 on the CPU as a
+    library cross-check of the unmasked / prefix-masked attention;
+  * invariants of softmax attention (single key, constant V, permutations,
+    shifts of all keys, Q = 0, one-hot limit, linearity in V, lse consistency).
+"""
+
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+from tests import brute
+
+
+def _rng(seed):
+    return np.random.default_rng(seed)
+
+
+# ----------------------------------------------------------------- rotary ---
+
+def check_rope_unit_vectors(rope_fn, spec_cls):
+    """A unit vector in the first channel of an axis block, at a token whose
+    coordinate on that axis is p, becomes (cos p, sin p) on that pair (j = 0,
+    frequency 1); the other axes' blocks are untouched."""
+    grid = (3, 4, 5)
+    dims = (4, 4, 4)
+    for mode in (0, 1):
+        spec = spec_cls(grid=grid, dims=dims, theta=10000.0, pair_mode=mode)
+        for axis, (t, h, w) in enumerate([(2, 0, 0), (0, 3, 0), (0, 0, 4)]):
+            n = (t * grid[1] + h) * grid[2] + w
+            p = (t, h, w)[axis]
+            off = sum(dims[:axis])
+            partner = off + 1 if mode == 0 else off + dims[axis] // 2
+            x = np.zeros((1, n + 1, 1, 12))
+            x[0, n, 0, off] = 1.0
+            y = rope_fn(x, spec)[0, n, 0]
+            exp = np.zeros(12)
+            exp[off] = math.cos(p)
+            exp[partner] = math.sin(p)
+            assert np.allclose(y, exp, atol=1e-15), (mode, axis, y, exp)
+
+
+def check_rope_known_frequency(rope_fn, spec_cls):
+    """theta = 1e4, d_t = 44: pair j = 11 of the time block has frequency
+    1e4 ** (-22/44) = 0.01, so a unit vector there turns by 0.01 * t."""
+    spec = spec_cls(grid=(21, 2, 3), dims=(44, 42, 42), theta=10000.0, pair_mode=0)
+    t = 17
+    n = t * 2 * 3
+    x = np.zeros((1, n + 1, 1, 128))
+    x[0, n, 0, 22] = 1.0
+    y = rope_fn(x, spec)[0, n, 0]
+    assert abs(y[22] - math.cos(0.17)) < 1e-15 and abs(y[23] - math.sin(0.17)) < 1e-15, y[20:26]
+    assert np.count_nonzero(np.abs(y) > 1e-15) == 2
+
+
+def check_rope_identities(rope_fn, spec_cls):
+    rng = _rng(7)
+    spec = spec_cls(grid=(3, 4, 5), dims=(44, 42, 42), theta=10000.0, pair_mode=0)
+    L = 70  # 60 grid tokens + 10 appended tokens
+    x = rng.standard_normal((2, L, 3, 128))
+    y = rope_fn(x, spec)
+    # origin token is unchanged, tokens beyond the grid are unchanged
+    assert np.array_equal(y[:, 0], x[:, 0])
+    assert np.array_equal(y[:, 60:], x[:, 60:])
+    # every channel pair keeps its length
+    for mode in (0, 1):
+        s = spec_cls(grid=spec.grid, dims=spec.dims, theta=spec.theta, pair_mode=mode)
+        yy = rope_fn(x, s)
+        off = 0
+        for da in s.dims:
+            for j in range(da // 2):
+                c0, c1 = (off + 2 * j, off + 2 * j + 1) if mode == 0 else (off + j, off + da // 2 + j)
+                n0 = x[..., c0] ** 2 + x[..., c1] ** 2
+                n1 = yy[..., c0] ** 2 + yy[..., c1] ** 2
+                assert np.allclose(n0, n1, rtol=1e-13, atol=1e-13)
+            off += da
+
+
+def check_rope_relative(rope_fn, spec_cls):
+    """<R(p) q, R(p') k> depends only on p - p': shifting both tokens by the
+    same step along any one axis leaves the inner product unchanged."""
+    rng = _rng(11)
+    grid = (4, 5, 6)
+    T, Hp, Wp = grid
+    for mode in (0, 1):
+        spec = spec_cls(grid=grid, dims=(44, 42, 42), theta=10000.0, pair_mode=mode)
+        L = T * Hp * Wp
+        q = rng.standard_normal(128)
+        k = rng.standard_normal(128)
+        x = np.zeros((1, L, 2, 128))
+        x[0, :, 0] = q
+        x[0, :, 1] = k
+        y = rope_fn(x, spec)
+
+        def tok(t, h, w):
+            return (t * Hp + h) * Wp + w
+
+        for (a, b), shift in [(((0, 1, 2), (2, 3, 0)), (1, 0, 0)),
+                              (((1, 0, 1), (0, 3, 2)), (0, 1, 0)),
+                              (((2, 2, 0), (1, 1, 3)), (0, 0, 2))]:
+            a2 = tuple(a[i] + shift[i] for i in range(3))
+            b2 = tuple(b[i] + shift[i] for i in range(3))
+            s1 = y[0, tok(*a), 0] @ y[0, tok(*b), 1]
+            s2 = y[0, tok(*a2), 0] @ y[0, tok(*b2), 1]
+            assert abs(s1 - s2) < 1e-11, (mode, a, b, shift, s1, s2)
+        # and it does change with the relative offset (the rotation is not trivial)
+        s_same = y[0, tok(1, 1, 1), 0] @ y[0, tok(1, 1, 1), 1]
+        s_off = y[0, tok(1, 1, 1), 0] @ y[0, tok(1, 1, 2), 1]
+        assert abs(s_same - q @ k) < 1e-11
+        assert abs(s_off - q @ k) > 1e-6
+
+
+def check_rope_brute(rope_fn, spec_cls):
+    rng = _rng(3)
+    for mode in (0, 1):
+        for grid, dims in [((2, 3, 2), (4, 4, 4)), ((1, 1, 7), (2, 4, 6)), ((3, 2, 2), (6, 2, 4))]:
+            spec = spec_cls(grid=grid, dims=dims, theta=100.0, pair_mode=mode)
+            L = grid[0] * grid[1] * grid[2] + 3
+            d = sum(dims)
+            x = rng.standard_normal((1, L, 2, d))
+            y = rope_fn(x, spec)
+            for n in range(L):
+                for h in range(2):
+                    yb = brute.rope_row(list(x[0, n, h]), n, grid, dims, 100.0, mode)
+                    assert np.allclose(y[0, n, h], yb, rtol=1e-13, atol=1e-13), (mode, grid, n)
+
+
+# -------------------------------------------------------------- attention ---
+
+def _tiny_case(rng, B=2, Lq=7, Lk=9, H=2, d=12):
+    q = rng.standard_normal((B, Lq, H, d))
+    k = rng.standard_normal((B, Lk, H, d))
+    v = rng.standard_normal((B, Lk, H, d))
+    return q, k, v
+
+
+def check_attn_brute(attn_fn, spec_cls):
+    rng = _rng(5)
+    for with_rope in (False, True):
+        for lv in (None, [9, 4], [1, 0], [12, 3]):
+            q, k, v = _tiny_case(rng)
+            spec = spec_cls(grid=(2, 2, 2), dims=(4, 4, 4), theta=100.0, pair_mode=0) if with_rope else None
+            o, lse = attn_fn(q, k, v, 0.37, kv_valid_len=lv, rope=spec)
+            rope = (spec.grid, spec.dims, spec.theta, spec.pair_mode) if with_rope else None
+            ob, lb = brute.attention(q.tolist(), k.tolist(), v.tolist(), 0.37, kv_valid_len=lv, rope=rope)
+            ob = np.array(ob)
+            lb = np.array(lb)
+            assert np.allclose(o, ob, rtol=1e-12, atol=1e-12), (with_rope, lv)
+            fin = np.isfinite(lb)
+            assert np.array_equal(fin, np.isfinite(lse))
+            assert np.allclose(lse[fin], lb[fin], rtol=1e-12, atol=1e-12)
+
+
+def check_attn_torch(attn_fn):
+    import torch
+
+    rng = _rng(9)
+    B, L, H, d = 2, 300, 3, 128
+    q, k, v = _tiny_case(rng, B=B, Lq=L, Lk=L, H=H, d=d)
+    scale = 1 / math.sqrt(d)
+    o, lse = attn_fn(q, k, v, scale)
+    tq, tk, tv = (torch.from_numpy(a).permute(0, 2, 1, 3) for a in (q, k, v))
+    ref = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, scale=scale).permute(0, 2, 1, 3).numpy()
+    assert np.allclose(o, ref, rtol=1e-11, atol=1e-12)
+    s = torch.einsum("bhqd,bhkd->bhqk", tq, tk) * scale
+    assert np.allclose(lse, torch.logsumexp(s, dim=-1).numpy(), rtol=1e-12, atol=1e-12)
+    # prefix mask == attention over the truncated key/value sequence
+    lv = [173, 300]
+    o2, _ = attn_fn(q, k, v, scale, kv_valid_len=lv)
+    for b in range(B):
+        r = torch.nn.functional.scaled_dot_product_attention(
+            tq[b:b + 1], tk[b:b + 1, :, :lv[b]], tv[b:b + 1, :, :lv[b]], scale=scale
+        ).permute(0, 2, 1, 3).numpy()
+        assert np.allclose(o2[b:b + 1], r, rtol=1e-11, atol=1e-12)
+
+
+def check_attn_invariants(attn_fn, spec_cls):
+    rng = _rng(13)
+    B, Lq, Lk, H, d = 2, 17, 23, 2, 16
+    q, k, v = _tiny_case(rng, B, Lq, Lk, H, d)
+    sc = 0.29
+    o, lse = attn_fn(q, k, v, sc)
+    # single valid key returns that value row exactly
+    o1, l1 = attn_fn(q, k, v, sc, kv_valid_len=[1, 1])
+    assert np.array_equal(o1, np.broadcast_to(v[:, :1], o1.shape))
+    s0 = sc * np.einsum("bqhd,bhd->bhq", q, k[:, 0])
+    assert np.allclose(l1, s0, rtol=1e-13, atol=1e-13)
+    # no valid key: zero output and -inf lse; lengths beyond Lk are clamped
+    oz, lz = attn_fn(q, k, v, sc, kv_valid_len=[0, Lk + 5])
+    assert np.all(oz[0] == 0) and np.all(np.isneginf(lz[0]))
+    assert np.allclose(oz[1], o[1], rtol=1e-14, atol=1e-14)
+    # constant V returns the constant
+    vc = np.broadcast_to(rng.standard_normal((1, 1, H, d)), v.shape).copy()
+    oc, _ = attn_fn(q, k, vc, sc)
+    assert np.allclose(oc, np.broadcast_to(vc[:, :1], oc.shape), rtol=1e-13, atol=1e-13)
+    # keys and values permuted together: same output
+    perm = rng.permutation(Lk)
+    op, lp = attn_fn(q, k[:, perm], v[:, perm], sc)
+    assert np.allclose(op, o, rtol=1e-12, atol=1e-13) and np.allclose(lp, lse, rtol=1e-13)
+    # queries permuted: output rows permuted
+    qp = rng.permutation(Lq)
+    oq, _ = attn_fn(q[:, qp], k, v, sc)
+    assert np.allclose(oq, o[:, qp], rtol=1e-13, atol=1e-14)
+    # the same vector added to every key: unchanged output (max subtraction, softmax shift)
+    u = rng.standard_normal((B, 1, H, d))
+    ou, _ = attn_fn(q, k + u, v, sc)
+    assert np.allclose(ou, o, rtol=1e-10, atol=1e-12)
+    # Q = 0 (or scale = 0) gives the mean of the valid value rows
+    for lv in (None, [5, 11]):
+        oq0, lq0 = attn_fn(np.zeros_like(q), k, v, sc, kv_valid_len=lv)
+        os0, _ = attn_fn(q, k, v, 0.0, kv_valid_len=lv)
+        for b in range(B):
+            n = Lk if lv is None else lv[b]
+            mean = v[b, :n].mean(axis=0)
+            assert np.allclose(oq0[b], np.broadcast_to(mean, oq0[b].shape), rtol=1e-13, atol=1e-14)
+            assert np.allclose(os0[b], np.broadcast_to(mean, os0[b].shape), rtol=1e-13, atol=1e-14)
+            assert np.allclose(lq0[b], math.log(n), rtol=1e-14)
+    # one-hot limit: with a large scale the output is the value row of the argmax
+    big = 1e4
+    ob, _ = attn_fn(q, k, v, big)
+    s = np.einsum("bqhd,bkhd->bhqk", q, k)
+    am = s.argmax(axis=-1)
+    for b in range(B):
+        for h in range(H):
+            assert np.allclose(ob[b, :, h], v[b, am[b, h], h], rtol=1e-9, atol=1e-9)
+    # linear in V
+    v2 = rng.standard_normal(v.shape)
+    ol, _ = attn_fn(q, k, 2.0 * v - 3.0 * v2, sc)
+    o2, _ = attn_fn(q, k, v2, sc)
+    assert np.allclose(ol, 2.0 * o - 3.0 * o2, rtol=1e-12, atol=1e-12)
+    # weights implied by lse sum to one: sum_j exp(s_ij - lse_i) == 1
+    w = np.exp(sc * s - lse[..., None])
+    assert np.allclose(w.sum(-1), 1.0, rtol=1e-13)
+    # and with rotary embedding, the output equals plain attention over rotated inputs
+    spec = spec_cls(grid=(2, 3, 3), dims=(6, 6, 4), theta=50.0, pair_mode=0)
+    orr, _ = attn_fn(q, k, v, sc, rope=spec)
+    assert not np.allclose(orr, o)
+
+
+ALL_ROPE_CHECKS = [check_rope_unit_vectors, check_rope_known_frequency, check_rope_identities,
+                   check_rope_relative, check_rope_brute]

@@ -1,0 +1,143 @@
+"""Plant plausible mistakes in (copies of) the oracle and show a pin catches each.
+
+Every mutation below is applied with monkeypatch to the oracle's own helpers,
+on the CPU; the pins in tests/pins.py must then fail.  This is evidence that
+the pins constrain the oracle's arithmetic, not only its shape.
+"""
+
+import numpy as np
+import pytest
+
+import oracle.attention as oa
+import oracle.rope3d as orr
+from oracle import RopeSpec, attn_ref, rope3d_ref
+from tests import pins
+
+
+def _pair_channels_sin_flipped(spec):
+    return [(a, j, c1, c0, om) for (a, j, c0, c1, om) in _ORIG_PAIRS(spec)]
+
+
+def _pair_channels_full_d(spec):
+    d = sum(spec.dims)
+    return [(a, j, c0, c1, float(spec.theta) ** (-2.0 * j / d)) for (a, j, c0, c1, _om) in _ORIG_PAIRS(spec)]
+
+
+def _pair_channels_mode_swapped(spec):
+    other = RopeSpec(grid=spec.grid, dims=spec.dims, theta=spec.theta, pair_mode=1 - spec.pair_mode)
+    return _ORIG_PAIRS(other)
+
+
+def _pair_channels_j_offset(spec):
+    return [(a, j, c0, c1, float(spec.theta) ** (-2.0 * (j + 1) / spec.dims[a])) for (a, j, c0, c1, _om) in _ORIG_PAIRS(spec)]
+
+
+def _coords_hw_swapped(n, grid):
+    c = _ORIG_COORDS(n, grid)
+    return c[..., [0, 2, 1]]
+
+
+def _coords_row_major_wrong(n, grid):
+    T, Hp, Wp = grid
+    n = np.asarray(n, dtype=np.int64)
+    return np.stack([n // (Hp * Wp), n % Hp, (n // Hp) % Wp], axis=-1)
+
+
+_ORIG_PAIRS = orr.pair_channels
+_ORIG_COORDS = orr.token_coords
+
+ROPE_MUTATIONS = {
+    "rotation_direction": ("pair_channels", _pair_channels_sin_flipped),
+    "frequency_over_full_d": ("pair_channels", _pair_channels_full_d),
+    "pair_convention": ("pair_channels", _pair_channels_mode_swapped),
+    "frequency_index_off_by_one": ("pair_channels", _pair_channels_j_offset),
+    "axes_h_w_swapped": ("token_coords", _coords_hw_swapped),
+    "token_flattening": ("token_coords", _coords_row_major_wrong),
+}
+
+
+def _any_rope_pin_fails():
+    for check in pins.ALL_ROPE_CHECKS:
+        try:
+            check(rope3d_ref, RopeSpec)
+        except AssertionError:
+            return True
+    return False
+
+
+@pytest.mark.parametrize("name", sorted(ROPE_MUTATIONS))
+def test_rope_mutation_is_caught(name, monkeypatch):
+    attr, fn = ROPE_MUTATIONS[name]
+    monkeypatch.setattr(orr, attr, fn)
+    assert _any_rope_pin_fails(), name
+
+
+_ORIG_BLOCK = oa._one_block
+_ORIG_LEN = oa._valid_lengths
+
+
+def _block_scale_twice(qb, kb, vb, scale):
+    return _ORIG_BLOCK(qb, kb, vb, scale * scale)
+
+
+def _block_softmax_wrong_axis(qb, kb, vb, scale):
+    s = scale * (qb @ kb.T)
+    m = s.max(axis=0)
+    e = np.exp(s - m[None, :])
+    l = e.sum(axis=0)
+    o = (e / l[None, :]) @ vb
+    return o, np.log(e.sum(axis=1)) + s.max(axis=1)
+
+
+def _block_lse_no_max(qb, kb, vb, scale):
+    o, lse = _ORIG_BLOCK(qb, kb, vb, scale)
+    s = scale * (qb @ kb.T)
+    return o, lse - s.max(axis=1)
+
+
+def _block_values_are_keys(qb, kb, vb, scale):
+    return _ORIG_BLOCK(qb, kb, kb, scale)
+
+
+def _block_no_normalisation(qb, kb, vb, scale):
+    s = scale * (qb @ kb.T)
+    m = s.max(axis=1)
+    e = np.exp(s - m[:, None])
+    return e @ vb, m + np.log(e.sum(axis=1))
+
+
+def _len_off_by_one(kv, B, Lk):
+    return np.clip(_ORIG_LEN(kv, B, Lk) + 1, 0, Lk)
+
+
+def _len_ignored(kv, B, Lk):
+    return np.full(B, Lk, dtype=np.int64)
+
+
+ATTN_MUTATIONS = {
+    "scale_applied_twice": ("_one_block", _block_scale_twice),
+    "softmax_over_queries": ("_one_block", _block_softmax_wrong_axis),
+    "lse_without_max": ("_one_block", _block_lse_no_max),
+    "values_are_keys": ("_one_block", _block_values_are_keys),
+    "missing_normalisation": ("_one_block", _block_no_normalisation),
+    "mask_off_by_one": ("_valid_lengths", _len_off_by_one),
+    "mask_ignored": ("_valid_lengths", _len_ignored),
+}
+
+
+def _any_attn_pin_fails():
+    for check in (lambda: pins.check_attn_brute(attn_ref, RopeSpec),
+                  lambda: pins.check_attn_torch(attn_ref),
+                  lambda: pins.check_attn_invariants(attn_ref, RopeSpec)):
+        try:
+            check()
+        except AssertionError:
+            return True
+    return False
+
+
+@pytest.mark.parametrize("name", sorted(ATTN_MUTATIONS))
+def test_attn_mutation_is_caught(name, monkeypatch):
+    attr, fn = ATTN_MUTATIONS[name]
+    monkeypatch.setattr(oa, attr, fn)
+    assert _any_attn_pin_fails(), name
