@@ -1,0 +1,135 @@
+/*
+ * vidax.h -- C ABI of the MI355X (gfx950) video-attention hot path.
+ *
+ * Two operations of a video diffusion transformer's attention block, over
+ * patchified multi-frame latent volumes (paper Section 2, "3D RoPE, 3D VAEs,
+ * and flash attention"; Section 4 and the full benchmark table give the
+ * workloads: tens of thousands of video tokens per sequence):
+ *
+ *   vidax_rope3d    3D rotary position embedding of query/key tokens over
+ *                   their (time, height, width) latent coordinates.
+ *   vidax_attn_fwd  non-causal softmax(scale * Q K^T) V, flash-attention style
+ *                   (the score matrix is never materialised), with the 3D
+ *                   rotation optionally fused into the Q/K loads and a
+ *                   per-batch valid-key prefix that replaces a dense mask
+ *                   (Appendix, porting-bug table, "Sharding, Parallelism &
+ *                   Custom Kernels": skip invalid key blocks instead of
+ *                   building a (B, H, Sq, Sk) mask).  The same entry point
+ *                   serves self-attention (Lq == Lk), text cross-attention
+ *                   (Lk = text length, no rotation) and joint video+text
+ *                   attention (rotation on the video prefix only).
+ *
+ * Conventions shared by every entry point
+ *   Layout    dense B x L x H x d ("BSHD"): element (b, n, h, c) sits at
+ *             ((b * L + n) * H + h) * d + c, bfloat16 storage.  Offsets are
+ *             64-bit inside the library.
+ *   Ownership the caller allocates and owns every buffer (device memory).  The
+ *             library never allocates, frees or synchronises, and keeps no
+ *             state between calls.  Work is enqueued on `stream`
+ *             (a hipStream_t; NULL = the legacy default stream).
+ *   Alignment q, k, v, o, x, y must be 16-byte aligned; lse and kv_valid_len
+ *             4-byte aligned.
+ *   Errors    arguments are validated synchronously; on any error nothing is
+ *             launched and a non-zero vidax_status is returned.  No C++
+ *             exception crosses this boundary.  Faults inside a kernel surface
+ *             at the caller's next synchronisation of `stream`.
+ */
+#ifndef VIDAX_H
+#define VIDAX_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define VIDAX_ABI_VERSION 1
+
+typedef enum vidax_status {
+  VIDAX_OK = 0,
+  VIDAX_ERR_INVALID_ARG = 1,  /* null/misaligned pointer, negative size, bad descriptor */
+  VIDAX_ERR_UNSUPPORTED = 2,  /* valid request outside what the kernels implement (e.g. d != 128) */
+  VIDAX_ERR_LAUNCH = 3        /* the HIP runtime rejected the launch */
+} vidax_status;
+
+/*
+ * 3D rotary embedding descriptor (paper Section 2: each family keeps its own
+ * convention, so the convention is data, not code).
+ *
+ *   Tokens n < grid_t * grid_h * grid_w are video tokens in patchify order,
+ *   n = (t * grid_h + h) * grid_w + w; later tokens (e.g. appended text) are
+ *   left unrotated.  The head dim is split into consecutive channel blocks of
+ *   widths dim_t, dim_h, dim_w (each even, >= 0, summing to d) for the t, h
+ *   and w coordinates.  In the block of axis a (offset o_a, width d_a), pair
+ *   j in [0, d_a/2) turns by phi = pos_a * theta^(-2j/d_a):
+ *     (x0, x1) -> (x0 cos phi - x1 sin phi, x0 sin phi + x1 cos phi),
+ *   with pair_mode 0 pairing channels (o_a+2j, o_a+2j+1) (interleaved) and
+ *   pair_mode 1 pairing (o_a+j, o_a+j+d_a/2) (half split).
+ *   Angles and the rotation are evaluated in fp32; results are rounded to
+ *   bfloat16 (nearest even).
+ */
+typedef struct vidax_rope3d_desc {
+  int32_t grid_t, grid_h, grid_w;
+  int32_t dim_t, dim_h, dim_w;
+  float theta;        /* > 0, finite; e.g. 10000 */
+  int32_t pair_mode;  /* 0 interleaved, 1 half split */
+} vidax_rope3d_desc;
+
+/*
+ * y = rope3d(x).  x, y: bf16 [B, L, H, d] (device).  x == y (in place) is
+ * allowed; other overlap is not.  Requires d == 128 (VIDAX_ERR_UNSUPPORTED
+ * otherwise), 1 <= grid_t*grid_h*grid_w <= L, B, L, H >= 0 (zero-sized calls
+ * are no-ops).  `rope` is a host pointer and must not be NULL.
+ */
+vidax_status vidax_rope3d(const void* x, void* y, int32_t B, int32_t L, int32_t H, int32_t d,
+                          const vidax_rope3d_desc* rope, hipStream_t stream);
+
+/*
+ * o = softmax(scale * rope(q) rope(k)^T + mask) v, per batch b and head h.
+ *
+ *   q, o : bf16 [B, Lq, H, d] (device);  k, v : bf16 [B, Lk, H, d] (device).
+ *   lse  : fp32 [B, H, Lq] natural-log sum-exp of the scaled scores of every
+ *          query row (device), or NULL to skip it.
+ *   scale: multiplies q.k (e.g. 1/sqrt(d) in fp32).
+ *   kv_valid_len: int32 [B] on the device, or NULL (= Lk for every batch).
+ *          Lv_b = clamp(kv_valid_len[b], 0, Lk): every query of batch b sees
+ *          keys [0, Lv_b) only.  Rows with Lv_b = 0 produce o = 0, lse = -inf.
+ *   rope : host pointer to a descriptor, or NULL for no rotation.  When given,
+ *          query token n and key token n are rotated as in vidax_rope3d
+ *          (fused into the loads; rotated values are rounded to bf16 before
+ *          the matrix products).  Requires pair_mode 0 and
+ *          grid_t*grid_h*grid_w <= min(Lq, Lk); the half-split convention is
+ *          served by rotating with vidax_rope3d first and passing rope = NULL.
+ *   All Lq rows are computed; there is no causal mask.  Matrix products run
+ *   on bf16 inputs with fp32 accumulation; the softmax is fp32.
+ *   Requires d == 128; o must not alias q, k or v.  B, H, Lq, Lk >= 0.
+ */
+vidax_status vidax_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
+                            int32_t B, int32_t H, int32_t Lq, int32_t Lk, int32_t d, float scale,
+                            const int32_t* kv_valid_len, const vidax_rope3d_desc* rope,
+                            hipStream_t stream);
+
+/*
+ * Same contract as vidax_attn_fwd, computed by a plain scalar fp32 kernel (one
+ * thread per query row, rotation evaluated on the fly, no matrix cores).  It
+ * exists as an independent second GPU implementation for cross-checks at
+ * small sizes; it also accepts pair_mode 1.  Slow: O(Lq * Lk * d) per head
+ * with no reuse.
+ */
+vidax_status vidax_attn_fwd_naive(const void* q, const void* k, const void* v, void* o, float* lse,
+                                  int32_t B, int32_t H, int32_t Lq, int32_t Lk, int32_t d, float scale,
+                                  const int32_t* kv_valid_len, const vidax_rope3d_desc* rope,
+                                  hipStream_t stream);
+
+/* Static string describing a status code (never NULL). */
+const char* vidax_status_string(vidax_status s);
+
+/* VIDAX_ABI_VERSION of the loaded library. */
+int32_t vidax_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VIDAX_H */

@@ -1,1 +1,166 @@
-"""MI355X-native 3D-RoPE + flash-attention forward (video-DiT attention hot path)."""
+"""MI355X-native 3D-RoPE + flash-attention forward (video-DiT attention hot path).
+
+Thin ctypes binding over ``libvidax.so`` (C ABI declared in include/vidax.h).
+This module only marshals arguments: torch provides device memory and the
+current HIP stream; every step of the computation runs in the library's
+kernels.  If the library has not been built the calls raise immediately --
+there is no fallback implementation.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libvidax.so")
+
+VIDAX_OK = 0
+_STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported configuration", 3: "kernel launch failed"}
+
+EXPORTED_SYMBOLS = (
+    "vidax_rope3d",
+    "vidax_attn_fwd",
+    "vidax_attn_fwd_naive",
+    "vidax_status_string",
+    "vidax_abi_version",
+)
+
+
+class VidaxError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn} returned {status} ({_STATUS.get(status, 'unknown')})")
+        self.status = status
+
+
+class RopeDesc(ctypes.Structure):
+    """Mirror of vidax_rope3d_desc."""
+
+    _fields_ = [
+        ("grid_t", ctypes.c_int32),
+        ("grid_h", ctypes.c_int32),
+        ("grid_w", ctypes.c_int32),
+        ("dim_t", ctypes.c_int32),
+        ("dim_h", ctypes.c_int32),
+        ("dim_w", ctypes.c_int32),
+        ("theta", ctypes.c_float),
+        ("pair_mode", ctypes.c_int32),
+    ]
+
+
+@dataclass(frozen=True)
+class Rope:
+    """3D rotary convention: token grid (T, Hp, Wp), channel split, theta, pairing."""
+
+    grid: tuple
+    dims: tuple = (44, 42, 42)
+    theta: float = 10000.0
+    pair_mode: int = 0
+
+    def desc(self) -> RopeDesc:
+        return RopeDesc(*self.grid, *self.dims, float(self.theta), int(self.pair_mode))
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libvidax.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with `python -m paper_2609_18077_amd.build` "
+                "(or __graft_entry__.build()); there is no fallback path"
+            )
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float
+        L.vidax_rope3d.argtypes = [vp, vp, i32, i32, i32, i32, ctypes.POINTER(RopeDesc), vp]
+        L.vidax_rope3d.restype = i32
+        for name in ("vidax_attn_fwd", "vidax_attn_fwd_naive"):
+            fn = getattr(L, name)
+            fn.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, f32, vp, ctypes.POINTER(RopeDesc), vp]
+            fn.restype = i32
+        L.vidax_status_string.argtypes = [i32]
+        L.vidax_status_string.restype = ctypes.c_char_p
+        L.vidax_abi_version.argtypes = []
+        L.vidax_abi_version.restype = i32
+        _lib = L
+    return _lib
+
+
+def _check(fn: str, status: int):
+    if status != VIDAX_OK:
+        raise VidaxError(fn, status)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _stream(stream):
+    import torch
+
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check_bshd(name, t):
+    import torch
+
+    if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous() or t.dim() != 4:
+        raise ValueError(f"{name} must be a contiguous bfloat16 [B, L, H, d] device tensor")
+
+
+def rope3d(x, rope: Rope, out=None, stream=None):
+    """Rotated copy of x (bf16 [B, L, H, d]); out may be x itself (in place)."""
+    import torch
+
+    _check_bshd("x", x)
+    y = torch.empty_like(x) if out is None else out
+    _check_bshd("out", y)
+    if y.shape != x.shape:
+        raise ValueError("out must have the shape of x")
+    B, L, H, d = x.shape
+    desc = rope.desc()
+    _check("vidax_rope3d", lib().vidax_rope3d(_ptr(x), _ptr(y), B, L, H, d, ctypes.byref(desc), _stream(stream)))
+    return y
+
+
+def _attn(fn_name, q, k, v, scale, kv_valid_len, rope, return_lse, out, stream):
+    import torch
+
+    for n, t in (("q", q), ("k", k), ("v", v)):
+        _check_bshd(n, t)
+    B, Lq, H, d = q.shape
+    if k.shape != v.shape or k.shape[0] != B or k.shape[2] != H or k.shape[3] != d:
+        raise ValueError("k and v must be [B, Lk, H, d] matching q's B, H, d")
+    Lk = k.shape[1]
+    if scale is None:
+        scale = float(torch.tensor(1.0 / d ** 0.5, dtype=torch.float32))
+    o = torch.empty_like(q) if out is None else out
+    _check_bshd("out", o)
+    lse = torch.empty((B, H, Lq), dtype=torch.float32, device=q.device) if return_lse else None
+    if kv_valid_len is not None:
+        if kv_valid_len.dtype != torch.int32 or not kv_valid_len.is_cuda or kv_valid_len.numel() != B:
+            raise ValueError("kv_valid_len must be an int32 device tensor of B elements")
+        kv_valid_len = kv_valid_len.contiguous()
+    desc = rope.desc() if rope is not None else None
+    fn = getattr(lib(), fn_name)
+    st = fn(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, H, Lq, Lk, d, float(scale),
+            _ptr(kv_valid_len), ctypes.byref(desc) if desc is not None else None, _stream(stream))
+    _check(fn_name, st)
+    return (o, lse) if return_lse else o
+
+
+def attn_fwd(q, k, v, scale=None, kv_valid_len=None, rope: Rope | None = None, return_lse=False, out=None,
+             stream=None):
+    """softmax(scale * rope(q) rope(k)^T) v on the matrix-core kernel (bf16 in/out, fp32 accumulate)."""
+    return _attn("vidax_attn_fwd", q, k, v, scale, kv_valid_len, rope, return_lse, out, stream)
+
+
+def attn_fwd_naive(q, k, v, scale=None, kv_valid_len=None, rope: Rope | None = None, return_lse=False, out=None,
+                   stream=None):
+    """Same contract on the scalar fp32 cross-check kernel (small sizes only)."""
+    return _attn("vidax_attn_fwd_naive", q, k, v, scale, kv_valid_len, rope, return_lse, out, stream)

@@ -1,0 +1,92 @@
+// Shared device/host definitions of the gfx950 kernels (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace vidax {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kHeadDim = 128;
+// Entries (cos, sin) of the per-workgroup rotary table kept in LDS.
+constexpr int kRopeTableMax = 4096;
+
+// Rotary parameters in the form the kernels consume (derived from
+// vidax_rope3d_desc by the host).
+struct RopeParams {
+  int enabled;
+  int gt, gh, gw;      // token grid
+  int dt, dh, dw;      // channel widths of the t, h, w blocks
+  int pair_mode;       // 0 interleaved, 1 half split
+  int n_rot;           // gt * gh * gw
+  int base1, base2;    // first table entry of the h and w axes
+  int n_entries;       // table entries: gt*dt/2 + gh*dh/2 + gw*dw/2
+  float log2_theta;
+};
+
+// ---------------------------------------------------------------- device ----
+
+__device__ __forceinline__ float bf16lo_to_f32(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf16hi_to_f32(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
+
+// fp32 -> bf16 bits, round to nearest even (hardware conversion on gfx950).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  __bf16 a = static_cast<__bf16>(lo);
+  __bf16 b = static_cast<__bf16>(hi);
+  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+}
+
+// Angle of table entry e: the entries of axis a are laid out [pos][j] with
+// d_a/2 entries per position; frequency theta^(-2j/d_a).
+__device__ __forceinline__ float2 rope_table_entry(const RopeParams& r, int e) {
+  int pos, j, da;
+  if (e < r.base1) {
+    int half = r.dt >> 1; pos = e / half; j = e - pos * half; da = r.dt;
+  } else if (e < r.base2) {
+    int half = r.dh >> 1; int f = e - r.base1; pos = f / half; j = f - pos * half; da = r.dh;
+  } else {
+    int half = r.dw >> 1; int f = e - r.base2; pos = f / half; j = f - pos * half; da = r.dw;
+  }
+  float omega = exp2f(-((float)(2 * j) / (float)da) * r.log2_theta);
+  float s, c;
+  sincosf((float)pos * omega, &s, &c);
+  return make_float2(c, s);
+}
+
+// Table entry of channel pair `pi` (interleaved numbering, pi in [0, 64)) at
+// coordinates (t, h, w): base of the pair's axis + pos * (d_a/2) + j.
+struct PairSlot {
+  int axis;   // 0, 1, 2
+  int base;   // base_a + j
+  int stride; // d_a / 2
+};
+
+__host__ __device__ inline PairSlot pair_slot(const RopeParams& r, int pi) {
+  PairSlot s;
+  int ht = r.dt >> 1, hh = r.dh >> 1;
+  if (pi < ht) {
+    s.axis = 0; s.base = pi; s.stride = ht;
+  } else if (pi < ht + hh) {
+    s.axis = 1; s.base = r.base1 + (pi - ht); s.stride = hh;
+  } else {
+    s.axis = 2; s.base = r.base2 + (pi - ht - hh); s.stride = r.dw >> 1;
+  }
+  return s;
+}
+
+}  // namespace vidax
+
+// Launchers implemented in the .hip files; called by the C ABI layer after
+// validation.  All pointers are device pointers; sizes already validated.
+namespace vidax {
+hipError_t launch_rope3d(const uint16_t* x, uint16_t* y, int B, int L, int H, const RopeParams& rp,
+                         hipStream_t stream);
+hipError_t launch_attn_naive(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o,
+                             float* lse, int B, int H, int Lq, int Lk, float scale,
+                             const int32_t* kv_valid_len, const RopeParams& rp, hipStream_t stream);
+hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o,
+                           float* lse, int B, int H, int Lq, int Lk, float scale,
+                           const int32_t* kv_valid_len, const RopeParams& rp, hipStream_t stream);
+}  // namespace vidax

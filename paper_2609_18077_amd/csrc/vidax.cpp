@@ -1,0 +1,159 @@
+// C ABI of libvidax: argument validation and dispatch to the gfx950 kernels.
+//
+// Every check runs before any HIP call, so a rejected call has no side effect
+// (and can be exercised on a machine without a GPU).
+#include <math.h>
+#include <stdint.h>
+
+#include "../../include/vidax.h"
+#include "common.hpp"
+
+namespace {
+
+using vidax::RopeParams;
+
+bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+// [p, p + bytes) and [q, q + bytes_q) overlap?
+bool overlaps(const void* p, uint64_t bytes, const void* q, uint64_t bytes_q) {
+  if (bytes == 0 || bytes_q == 0) return false;
+  const uintptr_t a0 = (uintptr_t)p, a1 = a0 + bytes;
+  const uintptr_t b0 = (uintptr_t)q, b1 = b0 + bytes_q;
+  return a0 < b1 && b0 < a1;
+}
+
+// Elements of a [B, L, H, d] tensor, or -1 if it does not fit in int64 byte offsets.
+int64_t numel4(int64_t B, int64_t L, int64_t H, int64_t d) {
+  const int64_t lim = INT64_C(1) << 60;
+  int64_t n = 1;
+  for (int64_t x : {B, L, H, d}) {
+    if (x != 0 && n > lim / x) return -1;
+    n *= x;
+  }
+  return n;
+}
+
+// Validates a rotary descriptor against the token counts it will see and
+// converts it.  `max_tokens`: rotated tokens must not exceed it.
+vidax_status make_rope(const vidax_rope3d_desc* r, int64_t max_tokens, int32_t d, RopeParams* out) {
+  if (r->grid_t < 1 || r->grid_h < 1 || r->grid_w < 1) return VIDAX_ERR_INVALID_ARG;
+  if (r->dim_t < 0 || r->dim_h < 0 || r->dim_w < 0) return VIDAX_ERR_INVALID_ARG;
+  if ((r->dim_t | r->dim_h | r->dim_w) & 1) return VIDAX_ERR_INVALID_ARG;
+  if ((int64_t)r->dim_t + r->dim_h + r->dim_w != d) return VIDAX_ERR_INVALID_ARG;
+  if (!(r->theta > 0.0f) || !isfinite(r->theta)) return VIDAX_ERR_INVALID_ARG;
+  if (r->pair_mode != 0 && r->pair_mode != 1) return VIDAX_ERR_INVALID_ARG;
+  const int64_t n_rot = (int64_t)r->grid_t * r->grid_h * r->grid_w;
+  if (n_rot > max_tokens) return VIDAX_ERR_INVALID_ARG;
+  const int64_t entries = (int64_t)r->grid_t * (r->dim_t / 2) + (int64_t)r->grid_h * (r->dim_h / 2) +
+                          (int64_t)r->grid_w * (r->dim_w / 2);
+  if (entries > vidax::kRopeTableMax) return VIDAX_ERR_UNSUPPORTED;
+  out->enabled = 1;
+  out->gt = r->grid_t;
+  out->gh = r->grid_h;
+  out->gw = r->grid_w;
+  out->dt = r->dim_t;
+  out->dh = r->dim_h;
+  out->dw = r->dim_w;
+  out->pair_mode = r->pair_mode;
+  out->n_rot = (int)n_rot;
+  out->base1 = r->grid_t * (r->dim_t / 2);
+  out->base2 = out->base1 + r->grid_h * (r->dim_h / 2);
+  out->n_entries = (int)entries;
+  out->log2_theta = log2f(r->theta);
+  return VIDAX_OK;
+}
+
+RopeParams no_rope() {
+  RopeParams p{};
+  p.enabled = 0;
+  p.gt = p.gh = p.gw = 1;
+  return p;
+}
+
+enum class AttnImpl { kMatrixCore, kNaive };
+
+vidax_status attn_common(AttnImpl impl, const void* q, const void* k, const void* v, void* o, float* lse,
+                         int32_t B, int32_t H, int32_t Lq, int32_t Lk, int32_t d, float scale,
+                         const int32_t* kv_valid_len, const vidax_rope3d_desc* rope, hipStream_t stream) {
+  if (B < 0 || H < 0 || Lq < 0 || Lk < 0 || d < 0) return VIDAX_ERR_INVALID_ARG;
+  if (!q || !k || !v || !o) return VIDAX_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16)) return VIDAX_ERR_INVALID_ARG;
+  if (lse && !aligned(lse, 4)) return VIDAX_ERR_INVALID_ARG;
+  if (kv_valid_len && !aligned(kv_valid_len, 4)) return VIDAX_ERR_INVALID_ARG;
+  if (!isfinite(scale)) return VIDAX_ERR_INVALID_ARG;
+  if (d != vidax::kHeadDim) return VIDAX_ERR_UNSUPPORTED;
+  const int64_t nq = numel4(B, Lq, H, d), nk = numel4(B, Lk, H, d);
+  if (nq < 0 || nk < 0) return VIDAX_ERR_INVALID_ARG;
+  const uint64_t qbytes = (uint64_t)nq * 2, kbytes = (uint64_t)nk * 2;
+  if (overlaps(o, qbytes, q, qbytes) || overlaps(o, qbytes, k, kbytes) || overlaps(o, qbytes, v, kbytes))
+    return VIDAX_ERR_INVALID_ARG;
+  if (lse && (overlaps(lse, (uint64_t)B * H * Lq * 4, o, qbytes) || overlaps(lse, (uint64_t)B * H * Lq * 4, q, qbytes)))
+    return VIDAX_ERR_INVALID_ARG;
+  RopeParams rp = no_rope();
+  if (rope) {
+    const vidax_status st = make_rope(rope, Lq < Lk ? Lq : Lk, d, &rp);
+    if (st != VIDAX_OK) return st;
+    if (impl == AttnImpl::kMatrixCore && rp.pair_mode != 0) return VIDAX_ERR_UNSUPPORTED;
+  }
+  // one workgroup per 256 (matrix core) or 64 (naive) query rows of each (b, h)
+  const int64_t rows = impl == AttnImpl::kMatrixCore ? 256 : 64;
+  const int64_t grid = ((int64_t)Lq + rows - 1) / rows * B * H;
+  if (grid > INT32_MAX) return VIDAX_ERR_UNSUPPORTED;
+  if (B == 0 || H == 0 || Lq == 0) return VIDAX_OK;
+
+  hipError_t e;
+  if (impl == AttnImpl::kMatrixCore)
+    e = vidax::launch_attn_fwd((const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, (uint16_t*)o, lse, B, H,
+                               Lq, Lk, scale, kv_valid_len, rp, stream);
+  else
+    e = vidax::launch_attn_naive((const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, (uint16_t*)o, lse, B,
+                                 H, Lq, Lk, scale, kv_valid_len, rp, stream);
+  return e == hipSuccess ? VIDAX_OK : VIDAX_ERR_LAUNCH;
+}
+
+}  // namespace
+
+extern "C" {
+
+vidax_status vidax_rope3d(const void* x, void* y, int32_t B, int32_t L, int32_t H, int32_t d,
+                          const vidax_rope3d_desc* rope, hipStream_t stream) {
+  if (B < 0 || L < 0 || H < 0 || d < 0) return VIDAX_ERR_INVALID_ARG;
+  if (!x || !y || !rope) return VIDAX_ERR_INVALID_ARG;
+  if (!aligned(x, 16) || !aligned(y, 16)) return VIDAX_ERR_INVALID_ARG;
+  if (d != vidax::kHeadDim) return VIDAX_ERR_UNSUPPORTED;
+  const int64_t n = numel4(B, L, H, d);
+  if (n < 0) return VIDAX_ERR_INVALID_ARG;
+  if (x != y && overlaps(x, (uint64_t)n * 2, y, (uint64_t)n * 2)) return VIDAX_ERR_INVALID_ARG;
+  RopeParams rp;
+  const vidax_status st = make_rope(rope, L, d, &rp);
+  if (st != VIDAX_OK) return st;
+  if (B == 0 || L == 0 || H == 0) return VIDAX_OK;
+  const hipError_t e = vidax::launch_rope3d((const uint16_t*)x, (uint16_t*)y, B, L, H, rp, stream);
+  return e == hipSuccess ? VIDAX_OK : VIDAX_ERR_LAUNCH;
+}
+
+vidax_status vidax_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int32_t B, int32_t H,
+                            int32_t Lq, int32_t Lk, int32_t d, float scale, const int32_t* kv_valid_len,
+                            const vidax_rope3d_desc* rope, hipStream_t stream) {
+  return attn_common(AttnImpl::kMatrixCore, q, k, v, o, lse, B, H, Lq, Lk, d, scale, kv_valid_len, rope, stream);
+}
+
+vidax_status vidax_attn_fwd_naive(const void* q, const void* k, const void* v, void* o, float* lse, int32_t B,
+                                  int32_t H, int32_t Lq, int32_t Lk, int32_t d, float scale,
+                                  const int32_t* kv_valid_len, const vidax_rope3d_desc* rope, hipStream_t stream) {
+  return attn_common(AttnImpl::kNaive, q, k, v, o, lse, B, H, Lq, Lk, d, scale, kv_valid_len, rope, stream);
+}
+
+const char* vidax_status_string(vidax_status s) {
+  switch (s) {
+    case VIDAX_OK: return "ok";
+    case VIDAX_ERR_INVALID_ARG: return "invalid argument";
+    case VIDAX_ERR_UNSUPPORTED: return "unsupported configuration";
+    case VIDAX_ERR_LAUNCH: return "kernel launch failed";
+  }
+  return "unknown status";
+}
+
+int32_t vidax_abi_version(void) { return VIDAX_ABI_VERSION; }
+
+}  // extern "C"

@@ -1,0 +1,280 @@
+"""GPU parity of the HIP path against the fp64 oracle (through the C ABI).
+
+Small and medium cases compare every output element; the full-size workloads
+(the launch configuration the benchmark times) compare sampled query rows,
+which the oracle computes exactly (rows are independent), and check a
+property over every output element: each output is a convex combination of
+the valid value rows, so every component lies within their per-channel range.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2609_18077_amd as vx
+from paper_2609_18077_amd import inputs
+from tests.gpu_util import (assert_lse, assert_parity, errors, lengths_dev, log, rope_of, spec_of, to_bits,
+                            to_dev)
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(w: inputs.Workload, q, k, v, lv, impl=vx.attn_fwd, lse=True):
+    import torch
+
+    qd, kd, vd = to_dev(q), to_dev(k), to_dev(v)
+    res = impl(qd, kd, vd, scale=w.scale, kv_valid_len=lengths_dev(lv), rope=rope_of(w), return_lse=lse)
+    torch.cuda.synchronize()
+    if lse:
+        o, l = res
+        return to_bits(o), l.cpu().numpy()
+    return to_bits(res), None
+
+
+def _oracle_full(w, q, k, v, lv):
+    dec = oracle.bf16_bits_to_f64
+    return oracle.attn_ref(dec(q), dec(k), dec(v), w.scale, kv_valid_len=lv, rope=spec_of(w), workers=8)
+
+
+def _full_case(w, impl=vx.attn_fwd, q=None, k=None, v=None, lv="default"):
+    if q is None:
+        q, k, v, lv0 = inputs.make_qkv(w)
+        if lv == "default":
+            lv = lv0
+    elif lv == "default":
+        lv = None
+    log(f"case {w.name} B{w.B} H{w.H} Lq{w.Lq} Lk{w.Lk} lv={None if lv is None else list(lv)} impl={impl.__name__}")
+    ob, lse = _run(w, q, k, v, lv, impl)
+    ro, rl = _oracle_full(w, q, k, v, lv)
+    assert_parity(ob, ro, w.name)
+    assert_lse(lse, rl, w.name)
+    return ob
+
+
+# ---------------------------------------------------------------- rope3d ----
+
+def _ulp_bf16(x):
+    m, e = np.frexp(np.abs(x))
+    return np.ldexp(1.0, np.maximum(e, -125) - 8)
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("inplace", [False, True])
+def test_rope3d_matches_oracle(mode, inplace):
+    import torch
+
+    grid = (3, 10, 30)  # 900 video tokens, then 100 unrotated tokens
+    x = inputs.bf16_tensor(11, 0, (2, 1000, 3, 128))
+    log(f"case rope3d mode={mode} inplace={inplace}")
+    xd = to_dev(x)
+    r = vx.Rope(grid=grid, dims=(44, 42, 42), theta=10000.0, pair_mode=mode)
+    y = vx.rope3d(xd, r, out=xd if inplace else None)
+    torch.cuda.synchronize()
+    got = oracle.bf16_bits_to_f64(to_bits(y))
+    ref = oracle.rope3d_ref(oracle.bf16_bits_to_f64(x), oracle.RopeSpec(grid=grid, pair_mode=mode))
+    err = np.abs(got - ref)
+    assert np.all(err <= _ulp_bf16(ref) + 1e-30), err.max()
+    exact = np.mean(to_bits(y) == oracle.f64_to_bf16_bits(ref))
+    log(f"  correctly rounded fraction {exact:.5f}")
+    assert exact > 0.995
+    assert np.array_equal(to_bits(y)[:, 900:], x[:, 900:])
+
+
+def test_rope3d_full_size_wan13b():
+    import torch
+
+    w = inputs.WORKLOADS["wan13b_480p"]
+    k = inputs.bf16_tensor(w.seed, inputs.T_K, (w.B, w.Lk, w.H, w.d), rms_norm=True)
+    log("case rope3d wan13b_480p K")
+    y = vx.rope3d(to_dev(k), rope_of(w))
+    torch.cuda.synchronize()
+    yb = to_bits(y)
+    rows = np.unique(np.r_[0, 1, 51, 52, 1559, 1560, w.Lk - 1, np.random.default_rng(0).integers(0, w.Lk, 300)])
+    ref = oracle.rope3d_ref(oracle.bf16_bits_to_f64(k[:, rows]), spec_of(w), token_index=rows)
+    got = oracle.bf16_bits_to_f64(yb[:, rows])
+    assert np.all(np.abs(got - ref) <= _ulp_bf16(ref) + 1e-30)
+
+
+# ------------------------------------------------------- attention: small ---
+
+def test_tiny_workload():
+    _full_case(inputs.WORKLOADS["tiny"])
+
+
+def test_tiny_workload_naive_kernel():
+    _full_case(inputs.WORKLOADS["tiny"], impl=vx.attn_fwd_naive)
+
+
+RAGGED = [
+    # several tiles with ragged tails in queries and keys, rotated prefix + unrotated suffix
+    inputs.custom("ragged_self", B=2, H=3, Lq=1000, Lk=1000, seed=21, grid=(2, 20, 24), kv_valid=("fixed", [1000, 517])),
+    # Lq != Lk with rotation (rotated tokens <= min(Lq, Lk))
+    inputs.custom("ragged_qk", B=1, H=2, Lq=777, Lk=1001, seed=22, grid=(1, 21, 37)),
+    # cross-attention shape, short keys, per-batch lengths incl. clamp above Lk
+    inputs.custom("cross_small", B=3, H=4, Lq=700, Lk=512, seed=23, kv_valid=("fixed", [64, 511, 900])),
+    # keys fewer than one tile, queries fewer than one wave
+    inputs.custom("few", B=1, H=1, Lq=5, Lk=3, seed=24),
+    inputs.custom("one", B=2, H=1, Lq=1, Lk=1, seed=25),
+    inputs.custom("tile_plus_one", B=1, H=2, Lq=257, Lk=65, seed=26, grid=(1, 5, 13)),
+]
+
+
+@pytest.mark.parametrize("w", RAGGED, ids=lambda w: w.name)
+def test_ragged_and_edge_shapes(w):
+    _full_case(w)
+
+
+@pytest.mark.parametrize("w", RAGGED[:3], ids=lambda w: w.name)
+def test_naive_kernel_agrees(w):
+    _full_case(w, impl=vx.attn_fwd_naive)
+
+
+def test_zero_and_single_valid_keys():
+    import torch
+
+    w = inputs.custom("lv_edge", B=4, H=2, Lq=300, Lk=200, seed=27, grid=(1, 10, 20))
+    q, k, v, _ = inputs.make_qkv(w)
+    lv = [0, 1, -5, 199]
+    log("case lv_edge", lv)
+    ob, lse = _run(w, q, k, v, lv)
+    # no valid key (0 or negative): zero output, -inf lse
+    assert np.all(ob[0] == 0) and np.all(ob[2] == 0)
+    assert np.all(np.isneginf(lse[0])) and np.all(np.isneginf(lse[2]))
+    # one valid key: the output is that key's value row, bit for bit
+    assert np.array_equal(ob[1], np.broadcast_to(v[1, :1], ob[1].shape))
+    ro, rl = _oracle_full(w, q, k, v, lv)
+    assert_parity(ob, ro, "lv_edge")
+    assert_lse(lse, rl, "lv_edge")
+    del torch
+
+
+def test_empty_calls_are_noops():
+    import torch
+
+    z = torch.zeros((0, 4, 2, 128), dtype=torch.bfloat16, device="cuda")
+    assert vx.attn_fwd(z, z, z).shape == z.shape
+    q = torch.zeros((1, 0, 2, 128), dtype=torch.bfloat16, device="cuda")
+    k = torch.zeros((1, 4, 2, 128), dtype=torch.bfloat16, device="cuda")
+    assert vx.attn_fwd(q, k, k).shape == q.shape
+    # no keys at all: zero output
+    q = torch.randn((1, 9, 2, 128), device="cuda").to(torch.bfloat16)
+    k = torch.zeros((1, 0, 2, 128), dtype=torch.bfloat16, device="cuda")
+    o, l = vx.attn_fwd(q, k, k, return_lse=True)
+    torch.cuda.synchronize()
+    assert torch.all(o == 0) and torch.all(torch.isneginf(l))
+
+
+@pytest.mark.parametrize("scale", [0.0, -0.05, 0.7])
+def test_scale_values(scale):
+    w = inputs.custom("scale", B=1, H=2, Lq=300, Lk=400, seed=28, grid=(1, 15, 20))
+    w = inputs.Workload(**{**w.__dict__, "name": f"scale{scale}"})
+    q, k, v, _ = inputs.make_qkv(w)
+    log(f"case scale {scale}")
+    import torch
+
+    res = vx.attn_fwd(to_dev(q), to_dev(k), to_dev(v), scale=scale, rope=rope_of(w), return_lse=True)
+    torch.cuda.synchronize()
+    ob, lse = to_bits(res[0]), res[1].cpu().numpy()
+    dec = oracle.bf16_bits_to_f64
+    ro, rl = oracle.attn_ref(dec(q), dec(k), dec(v), scale, rope=spec_of(w))
+    assert_parity(ob, ro, f"scale {scale}")
+    assert_lse(lse, rl, f"scale {scale}")
+
+
+def test_peaked_and_rescaling_logits():
+    """Scores that grow along the keys force a rescale of the running sum at
+    every tile; a large scale makes the softmax nearly one-hot."""
+    import torch
+
+    B, L, H, d = 1, 1000, 2, 128
+    rng = np.random.default_rng(29)
+    qf = np.zeros((B, L, H, d), np.float32)
+    qf[..., 0] = 1.0
+    qf[..., 1:] = 0.01 * rng.standard_normal((B, L, H, d - 1))
+    kf = 0.01 * rng.standard_normal((B, L, H, d)).astype(np.float32)
+    kf[..., 0] = 0.1 * np.arange(L)[None, :, None]            # increasing
+    kf[:, :, 1, 0] = 0.1 * np.arange(L)[::-1]                  # head 1: decreasing
+    vf = rng.standard_normal((B, L, H, d)).astype(np.float32)
+    q, k, v = (inputs.f32_to_bf16_bits(a).reshape(a.shape) for a in (qf, kf, vf))
+    dec = oracle.bf16_bits_to_f64
+    for scale in (1.0, 30.0):
+        log(f"case peaked scale={scale}")
+        o, l = vx.attn_fwd(to_dev(q), to_dev(k), to_dev(v), scale=scale, return_lse=True)
+        torch.cuda.synchronize()
+        ro, rl = oracle.attn_ref(dec(q), dec(k), dec(v), scale)
+        assert_parity(to_bits(o), ro, f"peaked {scale}")
+        assert_lse(l.cpu().numpy(), rl, f"peaked {scale}")
+
+
+def test_deterministic():
+    import torch
+
+    w = RAGGED[0]
+    q, k, v, lv = inputs.make_qkv(w)
+    qd, kd, vd, ld = to_dev(q), to_dev(k), to_dev(v), lengths_dev(lv)
+    log("case determinism")
+    outs = []
+    for _ in range(3):
+        o, l = vx.attn_fwd(qd, kd, vd, scale=w.scale, kv_valid_len=ld, rope=rope_of(w), return_lse=True)
+        torch.cuda.synchronize()
+        outs.append((to_bits(o), l.cpu().numpy()))
+    for o, l in outs[1:]:
+        assert np.array_equal(o, outs[0][0]) and np.array_equal(l, outs[0][1])
+
+
+# ----------------------------------------------------- full-size workloads ---
+
+def _sample_rows(L, rng, n=160):
+    fixed = [0, 1, 31, 32, 63, 64, 255, 256, 257, L // 2, L - 257, L - 256, L - 65, L - 64, L - 33, L - 2, L - 1]
+    fixed = [r for r in fixed if 0 <= r < L]
+    return np.unique(np.r_[fixed, rng.integers(0, L, n)])
+
+
+def _convex_bounds_ok(ob, v, lv, heads):
+    """Every output component lies in [min, max] of the valid value rows (per
+    batch, head, channel), up to one bf16 rounding of the output."""
+    got = oracle.bf16_bits_to_f64(ob)
+    for b in range(ob.shape[0]):
+        n = v.shape[1] if lv is None else int(np.clip(lv[b], 0, v.shape[1]))
+        vv = oracle.bf16_bits_to_f64(v[b, :n][:, heads])  # [n, Hs, d]
+        lo = vv.min(axis=0)
+        hi = vv.max(axis=0)
+        g = got[b][:, heads]
+        slack = 2.0 ** -8 * np.maximum(np.abs(lo), np.abs(hi)) + 1e-30
+        if not (np.all(g >= lo - slack) and np.all(g <= hi + slack)):
+            return False
+    return True
+
+
+@pytest.mark.parametrize("name,heads", [
+    ("wan13b_480p", None),
+    ("cross_text", None),
+    ("wan14b_720p", [0, 13, 26, 39]),
+    ("hunyuan_joint", [0, 11, 23]),
+])
+def test_full_size_workload_sampled(name, heads):
+    import torch
+
+    w = inputs.WORKLOADS[name]
+    log(f"case full-size {name}: generating inputs")
+    q, k, v, lv = inputs.make_qkv(w)
+    log(f"case full-size {name}: GPU call")
+    qd, kd, vd = to_dev(q), to_dev(k), to_dev(v)
+    o, l = vx.attn_fwd(qd, kd, vd, scale=w.scale, kv_valid_len=lengths_dev(lv), rope=rope_of(w), return_lse=True)
+    torch.cuda.synchronize()
+    ob = to_bits(o)
+    lse = l.cpu().numpy()
+    del qd, kd, vd, o, l
+    torch.cuda.empty_cache()
+    hs = list(range(w.H)) if heads is None else heads
+    assert np.all(np.isfinite(oracle.bf16_bits_to_f64(ob[:, :, hs])))
+    assert _convex_bounds_ok(ob, v, lv, hs)
+    rows = _sample_rows(w.Lq, np.random.default_rng(w.seed))
+    log(f"case full-size {name}: oracle on {len(rows)} rows x {len(hs)} heads")
+    dec = oracle.bf16_bits_to_f64
+    ro, rl = oracle.attn_ref_rows(dec(q[:, :, hs]), dec(k[:, :, hs]), dec(v[:, :, hs]), w.scale, rows,
+                                  kv_valid_len=lv, rope=spec_of(w), workers=8)
+    assert_parity(ob[:, rows][:, :, hs], ro, name)
+    assert_lse(lse[:, hs][:, :, rows], rl, name)
+    e = errors(ob[:, rows][:, :, hs], ro)
+    log(f"  {name}: {e}")

@@ -1,0 +1,102 @@
+"""The C-ABI library on the CPU: it loads, exports what include/vidax.h
+declares, and rejects invalid arguments synchronously (no kernel is launched,
+no GPU is needed)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_18077_amd as vx
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _header_functions():
+    src = open(os.path.join(ROOT, "include", "vidax.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(vidax_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function():
+    lib = vx.lib()
+    declared = _header_functions()
+    assert set(declared) == set(vx.EXPORTED_SYMBOLS), declared
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert lib.vidax_abi_version() == 1
+    for s, text in [(0, b"ok"), (1, b"invalid argument"), (2, b"unsupported configuration"), (3, b"kernel launch failed")]:
+        assert lib.vidax_status_string(s) == text
+    assert lib.vidax_status_string(99) == b"unknown status"
+
+
+P = 1 << 40  # fake, 16-byte aligned "device" addresses far apart; never dereferenced
+
+
+def _attn(fn="vidax_attn_fwd", q=P, k=2 * P, v=3 * P, o=4 * P, lse=None, B=1, H=2, Lq=64, Lk=64, d=128,
+          scale=0.088, kv=None, rope=None):
+    f = getattr(vx.lib(), fn)
+    return f(ctypes.c_void_p(q), ctypes.c_void_p(k), ctypes.c_void_p(v), ctypes.c_void_p(o),
+             ctypes.c_void_p(lse) if lse else None, B, H, Lq, Lk, d, scale,
+             ctypes.c_void_p(kv) if kv else None, ctypes.byref(rope) if rope is not None else None, None)
+
+
+@pytest.mark.parametrize("fn", ["vidax_attn_fwd", "vidax_attn_fwd_naive"])
+def test_attn_rejects_invalid_arguments(fn):
+    INV, UNS = 1, 2
+    assert _attn(fn, q=0) == INV
+    assert _attn(fn, o=0) == INV
+    assert _attn(fn, q=P + 8) == INV            # misaligned
+    assert _attn(fn, lse=5 * P + 2) == INV      # misaligned lse
+    assert _attn(fn, kv=6 * P + 1) == INV       # misaligned lengths
+    assert _attn(fn, B=-1) == INV
+    assert _attn(fn, Lk=-3) == INV
+    assert _attn(fn, scale=float("nan")) == INV
+    assert _attn(fn, scale=float("inf")) == INV
+    assert _attn(fn, d=64) == UNS
+    assert _attn(fn, o=P) == INV                # output aliases q
+    assert _attn(fn, o=2 * P + 4096) == INV     # output overlaps k
+    good = vx.Rope((1, 8, 8), (44, 42, 42)).desc()
+    bad = [vx.Rope((1, 8, 8), (44, 42, 40)).desc(),     # dims do not sum to d
+           vx.Rope((1, 8, 8), (43, 43, 42)).desc(),     # odd dims
+           vx.Rope((0, 8, 8), (44, 42, 42)).desc(),     # empty grid
+           vx.Rope((1, 8, 8), (44, 42, 42), theta=0.0).desc(),
+           vx.Rope((1, 8, 8), (44, 42, 42), theta=-1.0).desc(),
+           vx.Rope((1, 8, 8), (44, 42, 42), pair_mode=2).desc(),
+           vx.Rope((2, 8, 8), (44, 42, 42)).desc()]     # 128 rotated tokens > Lq = 64
+    for r in bad:
+        assert _attn(fn, rope=r) == INV
+    # rotary table larger than the on-chip table
+    assert _attn(fn, Lq=1 << 20, Lk=1 << 20, rope=vx.Rope((64, 128, 128), (44, 42, 42)).desc()) == UNS
+    del good
+
+
+def test_half_split_only_on_naive_and_rope3d():
+    r = vx.Rope((1, 8, 8), (44, 42, 42), pair_mode=1).desc()
+    assert _attn("vidax_attn_fwd", rope=r) == 2
+
+
+def test_rope3d_rejects_invalid_arguments():
+    f = vx.lib().vidax_rope3d
+    good = vx.Rope((2, 4, 8), (44, 42, 42)).desc()
+
+    def call(x=P, y=2 * P, B=1, L=64, H=2, d=128, rope=good):
+        return f(ctypes.c_void_p(x), ctypes.c_void_p(y), B, L, H, d,
+                 ctypes.byref(rope) if rope is not None else None, None)
+
+    assert call(rope=None) == 1
+    assert call(x=0) == 1
+    assert call(y=2 * P + 2) == 1
+    assert call(L=-1) == 1
+    assert call(d=96) == 2
+    assert call(L=63) == 1                    # 64 rotated tokens > L
+    assert call(y=P + 256) == 1               # partial overlap (in place is x == y)
+    assert call(rope=vx.Rope((2, 4, 8), (42, 42, 42)).desc()) == 1
+
+
+def test_binding_fails_loudly_without_library(monkeypatch):
+    monkeypatch.setattr(vx, "_lib", None)
+    monkeypatch.setattr(vx, "LIB_PATH", "/nonexistent/libvidax.so")
+    with pytest.raises(RuntimeError, match="no fallback"):
+        vx.lib()
