@@ -28,7 +28,8 @@
  *             state between calls.  Work is enqueued on `stream`
  *             (a hipStream_t; NULL = the legacy default stream).
  *   Alignment q, k, v, o, x, y must be 16-byte aligned; lse and kv_valid_len
- *             4-byte aligned.
+ *             4-byte aligned.  A tensor pointer may be NULL only when that
+ *             tensor has no elements.
  *   Errors    arguments are validated synchronously; on any error nothing is
  *             launched and a non-zero vidax_status is returned.  No C++
  *             exception crosses this boundary.  Faults inside a kernel surface

@@ -76,14 +76,15 @@ vidax_status attn_common(AttnImpl impl, const void* q, const void* k, const void
                          int32_t B, int32_t H, int32_t Lq, int32_t Lk, int32_t d, float scale,
                          const int32_t* kv_valid_len, const vidax_rope3d_desc* rope, hipStream_t stream) {
   if (B < 0 || H < 0 || Lq < 0 || Lk < 0 || d < 0) return VIDAX_ERR_INVALID_ARG;
-  if (!q || !k || !v || !o) return VIDAX_ERR_INVALID_ARG;
+  const int64_t nq = numel4(B, Lq, H, d), nk = numel4(B, Lk, H, d);
+  if (nq < 0 || nk < 0) return VIDAX_ERR_INVALID_ARG;
+  // a pointer may be NULL only when its tensor has no elements
+  if ((nq > 0 && (!q || !o)) || (nk > 0 && (!k || !v))) return VIDAX_ERR_INVALID_ARG;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16)) return VIDAX_ERR_INVALID_ARG;
   if (lse && !aligned(lse, 4)) return VIDAX_ERR_INVALID_ARG;
   if (kv_valid_len && !aligned(kv_valid_len, 4)) return VIDAX_ERR_INVALID_ARG;
   if (!isfinite(scale)) return VIDAX_ERR_INVALID_ARG;
   if (d != vidax::kHeadDim) return VIDAX_ERR_UNSUPPORTED;
-  const int64_t nq = numel4(B, Lq, H, d), nk = numel4(B, Lk, H, d);
-  if (nq < 0 || nk < 0) return VIDAX_ERR_INVALID_ARG;
   const uint64_t qbytes = (uint64_t)nq * 2, kbytes = (uint64_t)nk * 2;
   if (overlaps(o, qbytes, q, qbytes) || overlaps(o, qbytes, k, kbytes) || overlaps(o, qbytes, v, kbytes))
     return VIDAX_ERR_INVALID_ARG;
@@ -118,11 +119,12 @@ extern "C" {
 vidax_status vidax_rope3d(const void* x, void* y, int32_t B, int32_t L, int32_t H, int32_t d,
                           const vidax_rope3d_desc* rope, hipStream_t stream) {
   if (B < 0 || L < 0 || H < 0 || d < 0) return VIDAX_ERR_INVALID_ARG;
-  if (!x || !y || !rope) return VIDAX_ERR_INVALID_ARG;
-  if (!aligned(x, 16) || !aligned(y, 16)) return VIDAX_ERR_INVALID_ARG;
-  if (d != vidax::kHeadDim) return VIDAX_ERR_UNSUPPORTED;
+  if (!rope) return VIDAX_ERR_INVALID_ARG;
   const int64_t n = numel4(B, L, H, d);
   if (n < 0) return VIDAX_ERR_INVALID_ARG;
+  if (n > 0 && (!x || !y)) return VIDAX_ERR_INVALID_ARG;
+  if (!aligned(x, 16) || !aligned(y, 16)) return VIDAX_ERR_INVALID_ARG;
+  if (d != vidax::kHeadDim) return VIDAX_ERR_UNSUPPORTED;
   if (x != y && overlaps(x, (uint64_t)n * 2, y, (uint64_t)n * 2)) return VIDAX_ERR_INVALID_ARG;
   RopeParams rp;
   const vidax_status st = make_rope(rope, L, d, &rp);

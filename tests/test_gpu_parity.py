@@ -58,6 +58,37 @@ def _ulp_bf16(x):
     return np.ldexp(1.0, np.maximum(e, -125) - 8)
 
 
+def _pair_norm_and_angle(x, spec, rows):
+    """|(x0, x1)| of the rotary pair each channel belongs to, and that pair's
+    angle (0 for unrotated tokens), broadcast to x's [B, R, H, d] shape."""
+    from oracle.rope3d import pair_channels
+
+    d = x.shape[-1]
+    pairs = pair_channels(spec)
+    partner = np.empty(d, np.int64)
+    chan_pair = np.empty(d, np.int64)
+    for p, (_a, _j, c0, c1, _om) in enumerate(pairs):
+        partner[c0], partner[c1] = c1, c0
+        chan_pair[c0] = chan_pair[c1] = p
+    rows = np.asarray(rows)
+    phi = np.zeros((len(rows), len(pairs)))
+    rot = rows < spec.n_rot
+    if rot.any():
+        phi[rot] = oracle.rope_angles(spec, rows[rot])
+    ang = phi[:, chan_pair][None, :, None, :]
+    return np.sqrt(x * x + x[..., partner] ** 2), np.abs(ang)
+
+
+def _rope_bound(x, ref, spec, rows):
+    """One bf16 ulp of the result plus the fp32 evaluation error of the
+    rotation: the angle pos * omega and its sine/cosine carry a relative error
+    of a few 2^-24 (absolute ~|phi| 2^-22), and the two products of the pair
+    (magnitude <= |pair|) are rounded to 24 bits.  These only show where the
+    two products cancel; elsewhere the bf16 rounding dominates."""
+    norm, ang = _pair_norm_and_angle(x, spec, rows)
+    return _ulp_bf16(ref) + 2.0 ** -20 * norm * (1.0 + ang) + 1e-30
+
+
 @pytest.mark.parametrize("mode", [0, 1])
 @pytest.mark.parametrize("inplace", [False, True])
 def test_rope3d_matches_oracle(mode, inplace):
@@ -71,9 +102,11 @@ def test_rope3d_matches_oracle(mode, inplace):
     y = vx.rope3d(xd, r, out=xd if inplace else None)
     torch.cuda.synchronize()
     got = oracle.bf16_bits_to_f64(to_bits(y))
-    ref = oracle.rope3d_ref(oracle.bf16_bits_to_f64(x), oracle.RopeSpec(grid=grid, pair_mode=mode))
+    spec = oracle.RopeSpec(grid=grid, pair_mode=mode)
+    ref = oracle.rope3d_ref(oracle.bf16_bits_to_f64(x), spec)
     err = np.abs(got - ref)
-    assert np.all(err <= _ulp_bf16(ref) + 1e-30), err.max()
+    bound = _rope_bound(oracle.bf16_bits_to_f64(x), ref, spec, np.arange(x.shape[1]))
+    assert np.all(err <= bound), (err.max(), float((err / bound).max()))
     exact = np.mean(to_bits(y) == oracle.f64_to_bf16_bits(ref))
     log(f"  correctly rounded fraction {exact:.5f}")
     assert exact > 0.995
@@ -92,7 +125,7 @@ def test_rope3d_full_size_wan13b():
     rows = np.unique(np.r_[0, 1, 51, 52, 1559, 1560, w.Lk - 1, np.random.default_rng(0).integers(0, w.Lk, 300)])
     ref = oracle.rope3d_ref(oracle.bf16_bits_to_f64(k[:, rows]), spec_of(w), token_index=rows)
     got = oracle.bf16_bits_to_f64(yb[:, rows])
-    assert np.all(np.abs(got - ref) <= _ulp_bf16(ref) + 1e-30)
+    assert np.all(np.abs(got - ref) <= _rope_bound(oracle.bf16_bits_to_f64(k[:, rows]), ref, spec_of(w), rows))
 
 
 # ------------------------------------------------------- attention: small ---
@@ -166,19 +199,33 @@ def test_empty_calls_are_noops():
 
 @pytest.mark.parametrize("scale", [0.0, -0.05, 0.7])
 def test_scale_values(scale):
-    w = inputs.custom("scale", B=1, H=2, Lq=300, Lk=400, seed=28, grid=(1, 15, 20))
-    w = inputs.Workload(**{**w.__dict__, "name": f"scale{scale}"})
-    q, k, v, _ = inputs.make_qkv(w)
-    log(f"case scale {scale}")
+    """Zero, negative and large scales.  The kernel rounds the rotated query
+    and key to bf16 before the products (as documented); with a large scale
+    the logits are large and that input rounding dominates, so the reference
+    here is the oracle's attention over the oracle's rotated inputs rounded to
+    bf16 -- the remaining difference is the kernel's own arithmetic."""
     import torch
 
+    w = inputs.custom(f"scale{scale}", B=1, H=2, Lq=300, Lk=400, seed=28, grid=(1, 15, 20))
+    q, k, v, _ = inputs.make_qkv(w)
+    log(f"case scale {scale}")
     res = vx.attn_fwd(to_dev(q), to_dev(k), to_dev(v), scale=scale, rope=rope_of(w), return_lse=True)
     torch.cuda.synchronize()
     ob, lse = to_bits(res[0]), res[1].cpu().numpy()
     dec = oracle.bf16_bits_to_f64
-    ro, rl = oracle.attn_ref(dec(q), dec(k), dec(v), scale, rope=spec_of(w))
-    assert_parity(ob, ro, f"scale {scale}")
+    spec = spec_of(w)
+    qr = dec(oracle.f64_to_bf16_bits(oracle.rope3d_ref(dec(q), spec)))
+    kr = dec(oracle.f64_to_bf16_bits(oracle.rope3d_ref(dec(k), spec)))
+    ro, rl = oracle.attn_ref(qr, kr, dec(v), scale)
+    assert_parity(ob, ro, f"scale {scale} vs rounded rotated inputs")
     assert_lse(lse, rl, f"scale {scale}")
+    # against the exact oracle: same contract where the logits are moderate
+    ro2, _ = oracle.attn_ref(dec(q), dec(k), dec(v), scale, rope=spec)
+    e = errors(ob, ro2)
+    log(f"  vs exact rotation: {e}")
+    assert e["rel_rms"] <= 1e-2
+    if abs(scale) <= 0.1:
+        assert_parity(ob, ro2, f"scale {scale} exact")
 
 
 def test_peaked_and_rescaling_logits():

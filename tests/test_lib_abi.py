@@ -47,6 +47,7 @@ def test_attn_rejects_invalid_arguments(fn):
     INV, UNS = 1, 2
     assert _attn(fn, q=0) == INV
     assert _attn(fn, o=0) == INV
+    assert _attn(fn, q=0, o=0, k=0, v=0, Lq=0, Lk=0) == 0  # empty: no-op, NULL allowed
     assert _attn(fn, q=P + 8) == INV            # misaligned
     assert _attn(fn, lse=5 * P + 2) == INV      # misaligned lse
     assert _attn(fn, kv=6 * P + 1) == INV       # misaligned lengths
@@ -87,6 +88,7 @@ def test_rope3d_rejects_invalid_arguments():
 
     assert call(rope=None) == 1
     assert call(x=0) == 1
+    assert call(x=0, y=0, L=0, rope=vx.Rope((1, 1, 1), (44, 42, 42)).desc()) == 1  # 1 rotated token > L = 0
     assert call(y=2 * P + 2) == 1
     assert call(L=-1) == 1
     assert call(d=96) == 2
