@@ -161,6 +161,8 @@ def main():
     ap.add_argument("--workload", default="wan13b_480p")
     ap.add_argument("--all", action="store_true", help="also time every workload (stderr + gpurun_out/bench_all.json)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
+                    help="only run one plain device copy of MIB MiB (rocprofv3 counter calibration) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the attention kernel runs whole on a single MI355X "
@@ -174,6 +176,16 @@ def main():
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
+
+    if args.calib_copy:
+        n = args.calib_copy << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] copied {n} bytes device to device")
+        return
 
     w = inputs.WORKLOADS[args.workload]
     r = time_gpu(w, args.steps, args.warmup)

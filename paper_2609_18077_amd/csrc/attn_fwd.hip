@@ -28,6 +28,16 @@
 // every exponent <= 2^8 and the result exact up to rounding.  Row sums add
 // the bf16-rounded p actually fed to the PV product (v_dot2 with ones).
 //
+// Rotary embedding: each workgroup builds an fp32 (cos, sin) table per (axis,
+// position, frequency) in LDS; each axis has one extra identity position used
+// by unrotated tokens.  A thread fetches the coefficients of the K rows it
+// will stage next at the start of a pipeline step, so the LDS latency of the
+// (scattered) table reads hides behind the matrix work, and rotates in fp32
+// when it writes the tile.
+//
+// Global loads use buffer resources whose record count ends at the last valid
+// key, so rows past kv_valid_len read as zero without any per-lane test.
+//
 // LDS (per workgroup): K tiles 2 x 16 KB and V tiles 2 x 16 KB (row-major,
 // 16-byte chunks XOR swizzled by row), rotary table <= 32 KB.
 #include "common.hpp"
@@ -41,6 +51,7 @@ constexpr int BN = 64;
 constexpr int NW = 8;
 constexpr int NT = NW * 64;
 constexpr float kRescaleThreshold = 8.0f;
+constexpr int kBufferFlags = 0x00020000;  // raw buffer, 32-bit data format
 
 struct AttnArgs {
   const uint16_t* q;
@@ -55,9 +66,14 @@ struct AttnArgs {
   float c2;     // |scale| * log2(e), or 1 when scale == 0
   float qsign;  // +1, -1, or 0 (scale == 0) applied to the rotated query
   RopeParams rp;
-  // mixed-radix increment of a key token index by BN: (dt, dh, dw) digits
-  int step_t, step_h, step_w;
+  // attention rotary table: axis a holds (G_a + 1) positions x d_a/2 pairs
+  int tbase1, tbase2, tentries;
+  uint32_t pos_step;  // packed (t, h, w) increment of BN tokens
+  uint32_t pos_sent;  // packed identity position (gt, gh, gw)
 };
+
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -74,28 +90,71 @@ __device__ __forceinline__ float wave_half_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// Rotates the 4 interleaved pairs of one 16-byte chunk with table entries.
-__device__ __forceinline__ uint4 rotate_chunk(uint4 v, const float2* __restrict__ tab, const int idx[4]) {
-  uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    const float2 cs = tab[idx[p]];
-    const float x0 = bf16lo_to_f32(w[p]);
-    const float x1 = bf16hi_to_f32(w[p]);
-    w[p] = pack_bf16x2(fmaf(x0, cs.x, -x1 * cs.y), fmaf(x0, cs.y, x1 * cs.x));
-  }
-  return make_uint4(w[0], w[1], w[2], w[3]);
-}
-
-__device__ __forceinline__ int sel_pos(int axis, int t, int h, int w) {
-  return axis == 0 ? t : (axis == 1 ? h : w);
-}
-
-typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-
 __device__ __forceinline__ i16x4 lds_read_tr16(const uint16_t* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p));
+}
+
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c, false);
+}
+
+// Rotates one interleaved bf16 pair (x0 low, x1 high) by (cos, sin) in fp32.
+__device__ __forceinline__ uint32_t rotate_pair(uint32_t x, float2 cs) {
+  const float x0 = bf16lo_to_f32(x), x1 = bf16hi_to_f32(x);
+  return pack_bf16x2(fmaf(x0, cs.x, -x1 * cs.y), fmaf(x0, cs.y, x1 * cs.x));
+}
+
+// Table entry e of the attention kernel (see AttnArgs): position G_a of each
+// axis is the identity.
+__device__ float2 attn_table_entry(const AttnArgs& a, int e) {
+  const RopeParams& r = a.rp;
+  int f, half, da, g;
+  if (e < a.tbase1) { f = e; half = r.dt >> 1; da = r.dt; g = r.gt; }
+  else if (e < a.tbase2) { f = e - a.tbase1; half = r.dh >> 1; da = r.dh; g = r.gh; }
+  else { f = e - a.tbase2; half = r.dw >> 1; da = r.dw; g = r.gw; }
+  const int pos = f / half;
+  const int j = f - pos * half;
+  float c = 1.f, s = 0.f;
+  if (pos < g) {
+    const float omega = exp2f(-((float)(2 * j) / (float)da) * r.log2_theta);
+    sincosf((float)pos * omega, &s, &c);
+  }
+  return make_float2(c, s);
+}
+
+// Per channel pair: byte offset of its first table entry, byte stride per
+// position, and which coordinate of the packed (t << 22 | h << 11 | w)
+// position selects the row.  The w and h fields have one spare bit so a
+// BN-token step plus carry never overflows them.
+struct PairIdx {
+  int base, stride, shift, width;
+};
+constexpr int kEntryBytes = 8;
+
+__device__ __forceinline__ PairIdx pair_idx(const AttnArgs& a, int pi) {
+  const RopeParams& r = a.rp;
+  const int ht = r.dt >> 1, hh = r.dh >> 1;
+  PairIdx p;
+  if (pi < ht) { p.base = pi; p.stride = ht; p.shift = 22; p.width = 10; }
+  else if (pi < ht + hh) { p.base = a.tbase1 + pi - ht; p.stride = hh; p.shift = 11; p.width = 11; }
+  else { p.base = a.tbase2 + pi - ht - hh; p.stride = r.dw >> 1; p.shift = 0; p.width = 11; }
+  p.base *= kEntryBytes;
+  p.stride *= kEntryBytes;
+  return p;
+}
+
+// Table entry of pair p at packed position pos (24-bit multiply-add).
+__device__ __forceinline__ float2 table_entry(const float2* tab, const PairIdx& p, uint32_t pos) {
+  const uint32_t off = __umul24(__builtin_amdgcn_ubfe(pos, p.shift, p.width), (uint32_t)p.stride) + (uint32_t)p.base;
+  return *reinterpret_cast<const float2*>(reinterpret_cast<const char*>(tab) + off);
+}
+
+__device__ __forceinline__ uint32_t packed_pos(const AttnArgs& a, int n) {
+  if (n >= a.rp.n_rot) return a.pos_sent;
+  const int t = n / (a.rp.gh * a.rp.gw);
+  const int rem = n - t * a.rp.gh * a.rp.gw;
+  const int h = rem / a.rp.gw;
+  return ((uint32_t)t << 22) | ((uint32_t)h << 11) | (uint32_t)(rem - h * a.rp.gw);
 }
 
 // 16-byte chunk c of row r of a K tile / V tile
@@ -106,8 +165,7 @@ template <bool ROPE>
 __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t Ks[2][BN * D];
   __shared__ __attribute__((aligned(16))) uint16_t Vs[2][BN * D];
-  // rotary table plus one identity entry (cos 1, sin 0) for unrotated tokens
-  __shared__ float2 tab[ROPE ? kRopeTableMax + 1 : 1];
+  __shared__ float2 tab[ROPE ? kAttnTableMax : 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -131,8 +189,9 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
 
   int lv = a.Lk;
   if (a.kv_valid_len) lv = min(max(a.kv_valid_len[b], 0), a.Lk);
+  lv = __builtin_amdgcn_readfirstlane(lv);  // uniform: keeps buffer descriptors in SGPRs
 
-  const size_t tok = (size_t)a.H * D;
+  const int tok = a.H * D;  // elements between consecutive tokens
   const uint16_t* qbh = a.q + (size_t)b * a.Lq * tok + (size_t)h * D;
   const uint16_t* kbh = a.k + (size_t)b * a.Lk * tok + (size_t)h * D;
   const uint16_t* vbh = a.v + (size_t)b * a.Lk * tok + (size_t)h * D;
@@ -153,22 +212,16 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   }
 
   if (ROPE) {
-    for (int e = tid; e < a.rp.n_entries; e += NT) tab[e] = rope_table_entry(a.rp, e);
-    if (tid == 0) tab[a.rp.n_entries] = make_float2(1.f, 0.f);
+    for (int e = tid; e < a.tentries; e += NT) tab[e] = attn_table_entry(a, e);
     __syncthreads();
   }
 
   // ---- Q: lane holds query qrow, d-chunks 2s + hi (s = 0..7) as MFMA B operands
   bf16x8 qreg[8];
   {
-    int t = 0, hh = 0, w = 0;
-    const bool qrot = ROPE && qlive && qrow < a.rp.n_rot;
-    if (qrot) {
-      t = qrow / (a.rp.gh * a.rp.gw);
-      const int r = qrow - t * a.rp.gh * a.rp.gw;
-      hh = r / a.rp.gw;
-      w = r - hh * a.rp.gw;
-    }
+    const uint32_t qpos = ROPE ? packed_pos(a, qlive ? qrow : a.rp.n_rot) : 0u;
+    const uint32_t sgn = a.qsign < 0.f ? 0x80008000u : 0u;
+    const uint32_t keep = a.qsign == 0.f ? 0u : 0xffffffffu;
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       const int c = 2 * s + hi;
@@ -177,17 +230,8 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
       uint32_t wq[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
       for (int p = 0; p < 4; ++p) {
-        float x0 = bf16lo_to_f32(wq[p]);
-        float x1 = bf16hi_to_f32(wq[p]);
-        if (qrot) {
-          const PairSlot sl = pair_slot(a.rp, 4 * c + p);
-          const float2 cs = tab[sl.base + sel_pos(sl.axis, t, hh, w) * sl.stride];
-          const float y0 = fmaf(x0, cs.x, -x1 * cs.y);
-          const float y1 = fmaf(x0, cs.y, x1 * cs.x);
-          x0 = y0;
-          x1 = y1;
-        }
-        wq[p] = pack_bf16x2(x0 * a.qsign, x1 * a.qsign);
+        if (ROPE) wq[p] = rotate_pair(wq[p], table_entry(tab, pair_idx(a, 4 * c + p), qpos));
+        wq[p] = (wq[p] ^ sgn) & keep;
       }
       qreg[s] = __builtin_bit_cast(bf16x8, make_uint4(wq[0], wq[1], wq[2], wq[3]));
     }
@@ -196,63 +240,68 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   // ---- staging: thread owns chunk kc of rows kr0 and kr0 + 32 of every K and V tile
   const int kc = lane & 15;
   const int kr0 = (lane >> 4) + 4 * wave;
+  const int goff[2] = {(kr0 * tok + kc * 8) * 2, ((kr0 + 32) * tok + kc * 8) * 2};  // bytes from the tile's first row
 
   // rotary state of the two K rows (token index kr0 + 32 r + BN * tile)
-  int kslot_base[4], kslot_stride[4], kslot_axis[4];
-  int kt[2] = {0, 0}, kh[2] = {0, 0}, kw[2] = {0, 0};
+  PairIdx kpi[4];
+  uint32_t kpos[2] = {0u, 0u};
   if (ROPE) {
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const PairSlot sl = pair_slot(a.rp, 4 * kc + p);
-      kslot_base[p] = sl.base;
-      kslot_stride[p] = sl.stride;
-      kslot_axis[p] = sl.axis;
-    }
+    for (int p = 0; p < 4; ++p) kpi[p] = pair_idx(a, 4 * kc + p);
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
       const int n = kr0 + 32 * r;
-      kt[r] = n / (a.rp.gh * a.rp.gw);
-      const int rr = n - kt[r] * a.rp.gh * a.rp.gw;
-      kh[r] = rr / a.rp.gw;
-      kw[r] = rr - kh[r] * a.rp.gw;
+      const int t = n / (a.rp.gh * a.rp.gw);
+      const int rem = n - t * a.rp.gh * a.rp.gw;
+      const int hh = rem / a.rp.gw;
+      kpos[r] = ((uint32_t)t << 22) | ((uint32_t)hh << 11) | (uint32_t)(rem - hh * a.rp.gw);
     }
   }
 
   const int ntiles = (lv + BN - 1) / BN;
 
-  // Rows at or beyond lv read row lv - 1 (always valid) and are zeroed, so the
-  // loads carry no branch; tiles past the end are staged but never used.
+  // Rows of tile `tile` at or beyond lv lie outside the buffer's records and
+  // read as zero; tiles past the end read all zeros and are never used.
   auto load_rows = [&](const uint16_t* base, int tile, uint4 reg[2]) {
+    const int rows = min(max(lv - tile * BN, 0), BN);
+    const int nbytes = __builtin_amdgcn_readfirstlane(rows * tok * 2);  // uniform
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc((void*)(base + (size_t)tile * BN * tok), (short)0, nbytes, kBufferFlags);
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
-      const int n = tile * BN + kr0 + 32 * r;
-      const uint4 v = *reinterpret_cast<const uint4*>(base + (size_t)min(n, lv - 1) * tok + kc * 8);
-      const bool ok = n < lv;
-      reg[r] = make_uint4(ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u);
+      const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(rs, goff[r], 0, 0);
+      reg[r] = make_uint4(x[0], x[1], x[2], x[3]);
     }
   };
 
-  auto store_k = [&](int tile, uint16_t* buf, const uint4 reg[2]) {
+  // Coefficients for the two K rows of the next tile to be staged; advances
+  // the rows' packed coordinates by BN tokens.  Rows at or past the rotated
+  // prefix take the identity position.
+  auto fetch_coef = [&](int tile, float2 cs[2][4]) {
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
-      const int row = kr0 + 32 * r;
+      const uint32_t pos = tile * BN + kr0 + 32 * r < a.rp.n_rot ? kpos[r] : a.pos_sent;
+#pragma unroll
+      for (int p = 0; p < 4; ++p) cs[r][p] = table_entry(tab, kpi[p], pos);
+      // mixed-radix step; past the grid the t field may wrap, but those rows use pos_sent
+      uint32_t np = kpos[r] + a.pos_step;
+      if ((np & 2047u) >= (uint32_t)a.rp.gw) np += (1u << 11) - (uint32_t)a.rp.gw;
+      if (((np >> 11) & 2047u) >= (uint32_t)a.rp.gh) np += (1u << 22) - ((uint32_t)a.rp.gh << 11);
+      kpos[r] = np;
+    }
+  };
+
+  auto store_k = [&](uint16_t* buf, const uint4 reg[2], const float2 cs[2][4]) {
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
       uint4 kv = reg[r];
       if (ROPE) {
-        const bool rot = tile * BN + row < a.rp.n_rot;
-        int idx[4];
-#pragma unroll
-        for (int p = 0; p < 4; ++p)
-          idx[p] = rot ? kslot_base[p] + sel_pos(kslot_axis[p], kt[r], kh[r], kw[r]) * kslot_stride[p]
-                       : a.rp.n_entries;
-        kv = rotate_chunk(kv, tab, idx);
-        // advance this row's coordinates by BN tokens for the next tile
-        kw[r] += a.step_w;
-        kh[r] += a.step_h;
-        kt[r] += a.step_t;
-        if (kw[r] >= a.rp.gw) { kw[r] -= a.rp.gw; kh[r] += 1; }
-        if (kh[r] >= a.rp.gh) { kh[r] -= a.rp.gh; kt[r] += 1; }
+        kv.x = rotate_pair(kv.x, cs[r][0]);
+        kv.y = rotate_pair(kv.y, cs[r][1]);
+        kv.z = rotate_pair(kv.z, cs[r][2]);
+        kv.w = rotate_pair(kv.w, cs[r][3]);
       }
-      *reinterpret_cast<uint4*>(buf + k_off(row, kc)) = kv;
+      *reinterpret_cast<uint4*>(buf + k_off(kr0 + 32 * r, kc)) = kv;
     }
   };
 
@@ -293,16 +342,18 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   float mref = -INFINITY;  // reference max (log2 units), identical in both lane halves
   float lsum = 0.f;        // this lane half's partial sum of p
   const float c2 = a.c2;
-  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  const uint32_t ones = 0x3f803f80u;  // bf16 (1, 1)
 
   // row max of a score tile, rescale of the running output when it grew
   auto update_max = [&](const f32x16 s[2]) {
-    float mx = fmaxf(s[0][0], s[0][1]);
+    float m0 = fmaxf(s[0][0], s[0][1]);
+    float m1 = fmaxf(s[1][0], s[1][1]);
 #pragma unroll
-    for (int i = 2; i < 16; ++i) mx = fmaxf(mx, s[0][i]);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[1][i]);
-    mx = wave_half_max(mx) * c2;
+    for (int i = 2; i < 16; ++i) {
+      m0 = fmaxf(m0, s[0][i]);
+      m1 = fmaxf(m1, s[1][i]);
+    }
+    const float mx = wave_half_max(fmaxf(m0, m1)) * c2;
     if (__builtin_amdgcn_ballot_w64(mx > mref + kRescaleThreshold) != 0) {
       const float mnew = fmaxf(mref, mx);
       const float alpha = __builtin_amdgcn_exp2f(mref - mnew);
@@ -325,7 +376,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
         const float p0 = __builtin_amdgcn_exp2f(fmaf(s[ks >> 1][8 * (ks & 1) + e], c2, nm));
         const float p1 = __builtin_amdgcn_exp2f(fmaf(s[ks >> 1][8 * (ks & 1) + e + 1], c2, nm));
         pw[e >> 1] = pack_bf16x2(p0, p1);
-        lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pw[e >> 1]), ones, lsum, false);
+        lsum = dot2(pw[e >> 1], ones, lsum);
       }
       pop[ks] = __builtin_bit_cast(bf16x8, make_uint4(pw[0], pw[1], pw[2], pw[3]));
     }
@@ -347,12 +398,17 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   // ---- prologue: K0, V0 and K1 in LDS, scores of tile 0
   {
     uint4 k0[2], v0[2], k1[2];
+    float2 cs0[2][4], cs1[2][4];
     load_rows(kbh, 0, k0);
     load_rows(vbh, 0, v0);
     load_rows(kbh, 1, k1);
-    store_k(0, Ks[0], k0);
+    if (ROPE) {
+      fetch_coef(0, cs0);
+      fetch_coef(1, cs1);
+    }
+    store_k(Ks[0], k0, cs0);
     store_v(Vs[0], v0);
-    store_k(1, Ks[1], k1);
+    store_k(Ks[1], k1, cs1);
   }
   __syncthreads();
 
@@ -363,14 +419,16 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   // staging K_{j+2} and V_{j+1}
   auto step = [&](int j, f32x16 scur[2], f32x16 snext[2]) {
     uint4 kn[2], vn[2];
+    float2 cs[2][4];
     load_rows(kbh, j + 2, kn);
     load_rows(vbh, j + 1, vn);
+    if (ROPE) fetch_coef(j + 2, cs);
     update_max(scur);
     bf16x8 pop[4];
     qk(Ks[(j + 1) & 1], snext);
     softmax_p(scur, pop);
     pv(Vs[j & 1], pop);
-    store_k(j + 2, Ks[j & 1], kn);
+    store_k(Ks[j & 1], kn, cs);
     store_v(Vs[(j + 1) & 1], vn);
     __syncthreads();
   };
@@ -427,6 +485,14 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
 
 }  // namespace
 
+bool attn_rope_supported(const RopeParams& rp) {
+  if (!rp.enabled) return true;
+  if (rp.pair_mode != 0) return false;
+  if (rp.gw > kAttnGridHWMax || rp.gh > kAttnGridHWMax || rp.gt > kAttnGridTMax) return false;
+  const long entries = (long)(rp.gt + 1) * (rp.dt / 2) + (long)(rp.gh + 1) * (rp.dh / 2) + (long)(rp.gw + 1) * (rp.dw / 2);
+  return entries <= kAttnTableMax;
+}
+
 hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o,
                            float* lse, int B, int H, int Lq, int Lk, float scale,
                            const int32_t* kv_valid_len, const RopeParams& rp, hipStream_t stream) {
@@ -440,11 +506,15 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
   a.c2 = scale == 0.f ? 1.f : fabsf(scale) * 1.4426950408889634f;
   a.qsign = scale > 0.f ? 1.f : (scale < 0.f ? -1.f : 0.f);
   a.rp = rp;
-  a.step_t = a.step_h = a.step_w = 0;
+  a.tbase1 = a.tbase2 = a.tentries = 0;
+  a.pos_step = a.pos_sent = 0;
   if (rp.enabled) {
-    a.step_w = BN % rp.gw;
-    a.step_h = (BN / rp.gw) % rp.gh;
-    a.step_t = BN / (rp.gw * rp.gh);
+    a.tbase1 = (rp.gt + 1) * (rp.dt / 2);
+    a.tbase2 = a.tbase1 + (rp.gh + 1) * (rp.dh / 2);
+    a.tentries = a.tbase2 + (rp.gw + 1) * (rp.dw / 2);
+    const uint32_t sw = BN % rp.gw, sh = (BN / rp.gw) % rp.gh, st = BN / (rp.gw * rp.gh);
+    a.pos_step = (st << 22) | (sh << 11) | sw;
+    a.pos_sent = ((uint32_t)rp.gt << 22) | ((uint32_t)rp.gh << 11) | (uint32_t)rp.gw;
   }
   if (rp.enabled)
     hipLaunchKernelGGL(attn_fwd_kernel<true>, dim3((unsigned)nwg), dim3(NT), 0, stream, a);

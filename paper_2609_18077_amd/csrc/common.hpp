@@ -12,6 +12,11 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr int kHeadDim = 128;
 // Entries (cos, sin) of the per-workgroup rotary table kept in LDS.
 constexpr int kRopeTableMax = 4096;
+// The attention kernel's table has one extra identity position per axis and
+// packs a token's (t, h, w) into one word (w, h in 11-bit fields, t in 10).
+constexpr int kAttnTableMax = 4096;
+constexpr int kAttnGridHWMax = 1023;
+constexpr int kAttnGridTMax = 1023;
 
 // Rotary parameters in the form the kernels consume (derived from
 // vidax_rope3d_desc by the host).
@@ -31,11 +36,14 @@ struct RopeParams {
 __device__ __forceinline__ float bf16lo_to_f32(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float bf16hi_to_f32(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
 
-// fp32 -> bf16 bits, round to nearest even (hardware conversion on gfx950).
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Two fp32 -> packed bf16 pair (lo in bits 0-15), round to nearest even:
+// one v_cvt_pk_bf16_f32 on gfx950.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  __bf16 a = static_cast<__bf16>(lo);
-  __bf16 b = static_cast<__bf16>(hi);
-  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+  const f32x2 v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
 // Angle of table entry e: the entries of axis a are laid out [pos][j] with
@@ -86,6 +94,7 @@ hipError_t launch_rope3d(const uint16_t* x, uint16_t* y, int B, int L, int H, co
 hipError_t launch_attn_naive(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o,
                              float* lse, int B, int H, int Lq, int Lk, float scale,
                              const int32_t* kv_valid_len, const RopeParams& rp, hipStream_t stream);
+bool attn_rope_supported(const RopeParams& rp);
 hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o,
                            float* lse, int B, int H, int Lq, int Lk, float scale,
                            const int32_t* kv_valid_len, const RopeParams& rp, hipStream_t stream);

@@ -94,7 +94,7 @@ vidax_status attn_common(AttnImpl impl, const void* q, const void* k, const void
   if (rope) {
     const vidax_status st = make_rope(rope, Lq < Lk ? Lq : Lk, d, &rp);
     if (st != VIDAX_OK) return st;
-    if (impl == AttnImpl::kMatrixCore && rp.pair_mode != 0) return VIDAX_ERR_UNSUPPORTED;
+    if (impl == AttnImpl::kMatrixCore && !vidax::attn_rope_supported(rp)) return VIDAX_ERR_UNSUPPORTED;
   }
   // one workgroup per 256 (matrix core) or 64 (naive) query rows of each (b, h)
   const int64_t rows = impl == AttnImpl::kMatrixCore ? 256 : 64;
