@@ -8,7 +8,8 @@
 //   buffers each.  The loop is software pipelined: while the softmax of tile j
 //   runs on the vector ALUs, the matrix cores already compute the scores of
 //   tile j+1; while the PV products of tile j run, the threads write the next
-//   K tile (rotated) and V tile into the free buffers.  One barrier per tile.
+//   K tile (rotated) and V tile into the free buffers.  One barrier per tile;
+//   the two waves sharing a SIMD overlap each other's matrix and vector work.
 //
 // Matrix-core formulation (per wave, per key tile)
 //   S^T[64 keys x 32 queries] = K_tile * Q^T   (16 MFMAs: 2 key blocks x 8 d-steps)
@@ -38,8 +39,11 @@
 // Global loads use buffer resources whose record count ends at the last valid
 // key, so rows past kv_valid_len read as zero without any per-lane test.
 //
-// LDS (per workgroup): K tiles 2 x 16 KB and V tiles 2 x 16 KB (row-major,
-// 16-byte chunks XOR swizzled by row), rotary table <= 32 KB.
+// LDS (per workgroup): K tiles 2 x 17 KB and V tiles 2 x 20 KB, row-major with
+// padded rows (K: 256 + 16 bytes, V: 256 + 64 bytes) so that every operand
+// read and every staging write touches each bank at most the minimum number
+// of times, while operand offsets stay affine in the step index; rotary table
+// <= 32 KB.
 #include "common.hpp"
 
 namespace vidax {
@@ -127,7 +131,7 @@ __device__ float2 attn_table_entry(const AttnArgs& a, int e) {
 // position selects the row.  The w and h fields have one spare bit so a
 // BN-token step plus carry never overflows them.
 struct PairIdx {
-  int base, stride, shift, width;
+  int base, stride, shift;
 };
 constexpr int kEntryBytes = 8;
 
@@ -135,9 +139,9 @@ __device__ __forceinline__ PairIdx pair_idx(const AttnArgs& a, int pi) {
   const RopeParams& r = a.rp;
   const int ht = r.dt >> 1, hh = r.dh >> 1;
   PairIdx p;
-  if (pi < ht) { p.base = pi; p.stride = ht; p.shift = 22; p.width = 10; }
-  else if (pi < ht + hh) { p.base = a.tbase1 + pi - ht; p.stride = hh; p.shift = 11; p.width = 11; }
-  else { p.base = a.tbase2 + pi - ht - hh; p.stride = r.dw >> 1; p.shift = 0; p.width = 11; }
+  if (pi < ht) { p.base = pi; p.stride = ht; p.shift = 22; }
+  else if (pi < ht + hh) { p.base = a.tbase1 + pi - ht; p.stride = hh; p.shift = 11; }
+  else { p.base = a.tbase2 + pi - ht - hh; p.stride = r.dw >> 1; p.shift = 0; }
   p.base *= kEntryBytes;
   p.stride *= kEntryBytes;
   return p;
@@ -145,7 +149,8 @@ __device__ __forceinline__ PairIdx pair_idx(const AttnArgs& a, int pi) {
 
 // Table entry of pair p at packed position pos (24-bit multiply-add).
 __device__ __forceinline__ float2 table_entry(const float2* tab, const PairIdx& p, uint32_t pos) {
-  const uint32_t off = __umul24(__builtin_amdgcn_ubfe(pos, p.shift, p.width), (uint32_t)p.stride) + (uint32_t)p.base;
+  // the t field is the top 10 bits, so an 11-bit extract at offset 22 is exact
+  const uint32_t off = __umul24(__builtin_amdgcn_ubfe(pos, p.shift, 11), (uint32_t)p.stride) + (uint32_t)p.base;
   return *reinterpret_cast<const float2*>(reinterpret_cast<const char*>(tab) + off);
 }
 
@@ -157,14 +162,20 @@ __device__ __forceinline__ uint32_t packed_pos(const AttnArgs& a, int n) {
   return ((uint32_t)t << 22) | ((uint32_t)h << 11) | (uint32_t)(rem - h * a.rp.gw);
 }
 
-// 16-byte chunk c of row r of a K tile / V tile
-__device__ __forceinline__ int k_off(int r, int c) { return r * D + ((c ^ (r & 15)) << 3); }
-__device__ __forceinline__ int v_off(int r, int c) { return r * D + ((c ^ ((r & 3) << 2)) << 3); }
+// Element offset of 16-byte chunk c of row r of a K tile / V tile.  K rows of
+// 136 elements put row r's chunk c in 16-byte bank slot (r + c) mod 16; V rows
+// of 160 elements put it in slot (4 r + c) mod 16.
+constexpr int KROW = D + 8;
+constexpr int VROW = D + 32;
+constexpr int KTILE = BN * KROW;
+constexpr int VTILE = BN * VROW;
+__device__ __forceinline__ int k_off(int r, int c) { return r * KROW + (c << 3); }
+__device__ __forceinline__ int v_off(int r, int c) { return r * VROW + (c << 3); }
 
 template <bool ROPE>
 __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][BN * D];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[2][BN * D];
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KTILE];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[2][VTILE];
   __shared__ float2 tab[ROPE ? kAttnTableMax : 1];
 
   const int tid = threadIdx.x;
@@ -311,17 +322,13 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   };
 
   // per-lane LDS element offsets of the MFMA operands
-  int koff[8];
-#pragma unroll
-  for (int st = 0; st < 8; ++st) koff[st] = k_off(l32, 2 * st + hi);
+  const int koff = k_off(l32, hi);  // + 16 st for d-step st, + 32 KROW for key block 1
   // V^T via transposing reads: lane (h, g, i) = (hi, (lane >> 4) & 1, lane & 15)
   // reads 4 d-values of key row 16 ks + 8 r + 4 h + i/4 at d = 32 mb + 16 g + 4 (i & 3).
   const int vi = lane & 15;
   const int vg = (lane >> 4) & 1;
   const int vrow = 4 * hi + (vi >> 2);
-  int voff[4];
-#pragma unroll
-  for (int mb = 0; mb < 4; ++mb) voff[mb] = v_off(vrow, 4 * mb + 2 * vg + ((vi & 3) >> 1)) + 4 * (vi & 1);
+  const int voff = v_off(vrow, 2 * vg + ((vi & 3) >> 1)) + 4 * (vi & 1);  // + 32 mb for d block mb
 
   auto qk = [&](const uint16_t* kb, f32x16 s[2]) {
     s[0] = f32x16{};
@@ -330,7 +337,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
     for (int st = 0; st < 8; ++st) {
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk) {
-        const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kb + koff[st] + blk * 32 * D);
+        const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kb + koff + 16 * st + blk * 32 * KROW);
         s[blk] = mfma32(kop, qreg[st], s[blk]);
       }
     }
@@ -387,15 +394,15 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
     for (int ks = 0; ks < 4; ++ks) {
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb) {
-        const i16x4 lo = lds_read_tr16(vb + voff[mb] + (16 * ks) * D);
-        const i16x4 hi4 = lds_read_tr16(vb + voff[mb] + (16 * ks + 8) * D);
+        const i16x4 lo = lds_read_tr16(vb + voff + 32 * mb + (16 * ks) * VROW);
+        const i16x4 hi4 = lds_read_tr16(vb + voff + 32 * mb + (16 * ks + 8) * VROW);
         const bf16x8 vop = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
         oacc[mb] = mfma32(vop, pop[ks], oacc[mb]);
       }
     }
   };
 
-  // ---- prologue: K0, V0 and K1 in LDS, scores of tile 0
+  // ---- prologue: K_0, V_0 and K_1 in LDS (both halves), scores of tile 0
   {
     uint4 k0[2], v0[2], k1[2];
     float2 cs0[2][4], cs1[2][4];
@@ -415,8 +422,6 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   f32x16 sa[2], sb[2];
   qk(Ks[0], sa);
 
-  // one pipelined step: tile j's softmax + PV while tile j+1's scores run,
-  // staging K_{j+2} and V_{j+1}
   auto step = [&](int j, f32x16 scur[2], f32x16 snext[2]) {
     uint4 kn[2], vn[2];
     float2 cs[2][4];
@@ -444,8 +449,6 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
     ++j;
     slast = sb;
   }
-
-  // ---- last tile: mask keys >= lv, softmax, PV
   {
     f32x16 s[2] = {slast[0], slast[1]};
     if (j * BN + BN > lv) {
