@@ -24,10 +24,14 @@
 //
 // Softmax: p = exp2(s * c - m) with c = |scale| * log2 e in one FMA (the
 // rotated query is rounded to bf16 unscaled; a negative scale negates it, a
-// zero scale zeroes it).  The output/sum rescale is skipped until some row's
-// tile max exceeds its reference max by more than 8 (factor 256), which keeps
-// every exponent <= 2^8 and the result exact up to rounding.  Row sums add
-// the bf16-rounded p actually fed to the PV product (v_dot2 with ones).
+// zero scale zeroes it).  The reference m of a row is not the running max but
+// the max of the tile that last reset it: no per-tile max is computed.  A
+// tile whose row sum of p reaches 2^64 (or is not finite -- the first tile
+// always is, since m starts at -inf) resets m to the running max, rescales the
+// output and sum, and recomputes its p.  p therefore never exceeds 2^64, so
+// the bf16 P, fp32 sums and fp32 output accumulators cannot overflow, and the
+// result equals the usual online softmax up to rounding.  Row sums add the
+// bf16-rounded p actually fed to the PV product (v_dot2 with ones).
 //
 // Rotary embedding: each workgroup builds an fp32 (cos, sin) table per (axis,
 // position, frequency) in LDS; each axis has one extra identity position used
@@ -54,7 +58,7 @@ constexpr int BM = 256;
 constexpr int BN = 64;
 constexpr int NW = 8;
 constexpr int NT = NW * 64;
-constexpr float kRescaleThreshold = 8.0f;
+constexpr float kSumLimit = 18446744073709551616.0f;  // 2^64
 constexpr int kBufferFlags = 0x00020000;  // raw buffer, 32-bit data format
 
 struct AttnArgs {
@@ -351,30 +355,10 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   const float c2 = a.c2;
   const uint32_t ones = 0x3f803f80u;  // bf16 (1, 1)
 
-  // row max of a score tile, rescale of the running output when it grew
-  auto update_max = [&](const f32x16 s[2]) {
-    float m0 = fmaxf(s[0][0], s[0][1]);
-    float m1 = fmaxf(s[1][0], s[1][1]);
-#pragma unroll
-    for (int i = 2; i < 16; ++i) {
-      m0 = fmaxf(m0, s[0][i]);
-      m1 = fmaxf(m1, s[1][i]);
-    }
-    const float mx = wave_half_max(fmaxf(m0, m1)) * c2;
-    if (__builtin_amdgcn_ballot_w64(mx > mref + kRescaleThreshold) != 0) {
-      const float mnew = fmaxf(mref, mx);
-      const float alpha = __builtin_amdgcn_exp2f(mref - mnew);
-      lsum *= alpha;
-#pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) oacc[mb][i] *= alpha;
-      mref = mnew;
-    }
-  };
-
+  // p = exp2(s c - mref) as bf16 MFMA operands; returns this lane's sum of p
   auto softmax_p = [&](const f32x16 s[2], bf16x8 pop[4]) {
     const float nm = -mref;
+    float tsum = 0.f;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       uint32_t pw[4];
@@ -383,10 +367,36 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
         const float p0 = __builtin_amdgcn_exp2f(fmaf(s[ks >> 1][8 * (ks & 1) + e], c2, nm));
         const float p1 = __builtin_amdgcn_exp2f(fmaf(s[ks >> 1][8 * (ks & 1) + e + 1], c2, nm));
         pw[e >> 1] = pack_bf16x2(p0, p1);
-        lsum = dot2(pw[e >> 1], ones, lsum);
+        tsum = dot2(pw[e >> 1], ones, tsum);
       }
       pop[ks] = __builtin_bit_cast(bf16x8, make_uint4(pw[0], pw[1], pw[2], pw[3]));
     }
+    return tsum;
+  };
+
+  // probabilities of a score tile; resets the reference when a row's sum
+  // leaves [0, 2^64) (see the header)
+  auto softmax_tile = [&](const f32x16 s[2], bf16x8 pop[4]) {
+    float tsum = softmax_p(s, pop);
+    if (__builtin_amdgcn_ballot_w64(!(tsum < kSumLimit)) != 0) {
+      float m0 = fmaxf(s[0][0], s[0][1]);
+      float m1 = fmaxf(s[1][0], s[1][1]);
+#pragma unroll
+      for (int i = 2; i < 16; ++i) {
+        m0 = fmaxf(m0, s[0][i]);
+        m1 = fmaxf(m1, s[1][i]);
+      }
+      const float mnew = fmaxf(mref, wave_half_max(fmaxf(m0, m1)) * c2);
+      const float alpha = __builtin_amdgcn_exp2f(mref - mnew);
+      lsum *= alpha;
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) oacc[mb][i] *= alpha;
+      mref = mnew;
+      tsum = softmax_p(s, pop);
+    }
+    lsum += tsum;
   };
 
   auto pv = [&](const uint16_t* vb, const bf16x8 pop[4]) {
@@ -428,10 +438,9 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
     load_rows(kbh, j + 2, kn);
     load_rows(vbh, j + 1, vn);
     if (ROPE) fetch_coef(j + 2, cs);
-    update_max(scur);
-    bf16x8 pop[4];
     qk(Ks[(j + 1) & 1], snext);
-    softmax_p(scur, pop);
+    bf16x8 pop[4];
+    softmax_tile(scur, pop);
     pv(Vs[j & 1], pop);
     store_k(Ks[j & 1], kn, cs);
     store_v(Vs[(j + 1) & 1], vn);
@@ -460,9 +469,8 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
           if (key >= lv) s[blk][i] = -INFINITY;
         }
     }
-    update_max(s);
     bf16x8 pop[4];
-    softmax_p(s, pop);
+    softmax_tile(s, pop);
     pv(Vs[j & 1], pop);
   }
 
