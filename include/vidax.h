@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define VIDAX_ABI_VERSION 1
+#define VIDAX_ABI_VERSION 2
 
 typedef enum vidax_status {
   VIDAX_OK = 0,
@@ -73,8 +73,11 @@ typedef enum vidax_status {
 typedef struct vidax_rope3d_desc {
   int32_t grid_t, grid_h, grid_w;
   int32_t dim_t, dim_h, dim_w;
-  float theta;        /* > 0, finite; e.g. 10000 */
-  int32_t pair_mode;  /* 0 interleaved, 1 half split */
+  float theta;              /* > 0, finite; e.g. 10000 */
+  int32_t pair_mode;        /* 0 interleaved, 1 half split */
+  int32_t keys_prerotated;  /* attention only: 1 = k was already rotated (for
+                               instance by vidax_rope3d), rotate q only; 0 = rotate
+                               both inside the kernel.  vidax_rope3d ignores it. */
 } vidax_rope3d_desc;
 
 /*
@@ -99,9 +102,15 @@ vidax_status vidax_rope3d(const void* x, void* y, int32_t B, int32_t L, int32_t 
  *   rope : host pointer to a descriptor, or NULL for no rotation.  When given,
  *          query token n and key token n are rotated as in vidax_rope3d
  *          (fused into the loads; rotated values are rounded to bf16 before
- *          the matrix products).  Requires pair_mode 0 and
+ *          the matrix products).  With keys_prerotated = 1 only the queries
+ *          are rotated in the kernel and k must hold keys already rotated
+ *          with the same descriptor (vidax_rope3d): every query tile of a
+ *          head re-rotates every key tile in the fused form, so one
+ *          vidax_rope3d pass over k is cheaper at long sequence lengths.
+ *          Requires pair_mode 0, grid_t, grid_h, grid_w <= 1023, a rotary
+ *          table of at most 4096 entries (VIDAX_ERR_UNSUPPORTED otherwise) and
  *          grid_t*grid_h*grid_w <= min(Lq, Lk); the half-split convention is
- *          served by rotating with vidax_rope3d first and passing rope = NULL.
+ *          served by rotating q and k with vidax_rope3d and passing rope = NULL.
  *   All Lq rows are computed; there is no causal mask.  Matrix products run
  *   on bf16 inputs with fp32 accumulation; the softmax is fp32.
  *   Requires d == 128; o must not alias q, k or v.  B, H, Lq, Lk >= 0.

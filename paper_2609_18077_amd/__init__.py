@@ -46,6 +46,7 @@ class RopeDesc(ctypes.Structure):
         ("dim_w", ctypes.c_int32),
         ("theta", ctypes.c_float),
         ("pair_mode", ctypes.c_int32),
+        ("keys_prerotated", ctypes.c_int32),
     ]
 
 
@@ -57,9 +58,10 @@ class Rope:
     dims: tuple = (44, 42, 42)
     theta: float = 10000.0
     pair_mode: int = 0
+    keys_prerotated: bool = False  # attention: k already rotated (rotate q only)
 
     def desc(self) -> RopeDesc:
-        return RopeDesc(*self.grid, *self.dims, float(self.theta), int(self.pair_mode))
+        return RopeDesc(*self.grid, *self.dims, float(self.theta), int(self.pair_mode), int(self.keys_prerotated))
 
 
 _lib = None

@@ -176,7 +176,9 @@ constexpr int VTILE = BN * VROW;
 __device__ __forceinline__ int k_off(int r, int c) { return r * KROW + (c << 3); }
 __device__ __forceinline__ int v_off(int r, int c) { return r * VROW + (c << 3); }
 
-template <bool ROPE>
+// ROPE: rotate the queries (and build the table); ROPE_K: also rotate the keys
+// while staging them (false when the caller passes pre-rotated keys).
+template <bool ROPE, bool ROPE_K>
 __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KTILE];
   __shared__ __attribute__((aligned(16))) uint16_t Vs[2][VTILE];
@@ -260,7 +262,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   // rotary state of the two K rows (token index kr0 + 32 r + BN * tile)
   PairIdx kpi[4];
   uint32_t kpos[2] = {0u, 0u};
-  if (ROPE) {
+  if (ROPE_K) {
 #pragma unroll
     for (int p = 0; p < 4; ++p) kpi[p] = pair_idx(a, 4 * kc + p);
 #pragma unroll
@@ -310,7 +312,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
       uint4 kv = reg[r];
-      if (ROPE) {
+      if (ROPE_K) {
         kv.x = rotate_pair(kv.x, cs[r][0]);
         kv.y = rotate_pair(kv.y, cs[r][1]);
         kv.z = rotate_pair(kv.z, cs[r][2]);
@@ -419,7 +421,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
     load_rows(kbh, 0, k0);
     load_rows(vbh, 0, v0);
     load_rows(kbh, 1, k1);
-    if (ROPE) {
+    if (ROPE_K) {
       fetch_coef(0, cs0);
       fetch_coef(1, cs1);
     }
@@ -437,7 +439,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
     float2 cs[2][4];
     load_rows(kbh, j + 2, kn);
     load_rows(vbh, j + 1, vn);
-    if (ROPE) fetch_coef(j + 2, cs);
+    if (ROPE_K) fetch_coef(j + 2, cs);
     qk(Ks[(j + 1) & 1], snext);
     bf16x8 pop[4];
     softmax_tile(scur, pop);
@@ -527,10 +529,12 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
     a.pos_step = (st << 22) | (sh << 11) | sw;
     a.pos_sent = ((uint32_t)rp.gt << 22) | ((uint32_t)rp.gh << 11) | (uint32_t)rp.gw;
   }
-  if (rp.enabled)
-    hipLaunchKernelGGL(attn_fwd_kernel<true>, dim3((unsigned)nwg), dim3(NT), 0, stream, a);
+  if (rp.enabled && !rp.keys_prerotated)
+    hipLaunchKernelGGL((attn_fwd_kernel<true, true>), dim3((unsigned)nwg), dim3(NT), 0, stream, a);
+  else if (rp.enabled)
+    hipLaunchKernelGGL((attn_fwd_kernel<true, false>), dim3((unsigned)nwg), dim3(NT), 0, stream, a);
   else
-    hipLaunchKernelGGL(attn_fwd_kernel<false>, dim3((unsigned)nwg), dim3(NT), 0, stream, a);
+    hipLaunchKernelGGL((attn_fwd_kernel<false, false>), dim3((unsigned)nwg), dim3(NT), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -99,7 +99,7 @@ __global__ __launch_bounds__(kQ) void attn_naive_kernel(NaiveArgs a) {
       for (int e = threadIdx.x; e < kKeys * (kHeadDim / 2); e += kQ) {
         const int r = e / (kHeadDim / 2), p = e % (kHeadDim / 2);
         const int n = k0 + r;
-        if (n < lv && n < a.rp.n_rot) rotate_pair_direct(a.rp, ks[r], n, p);
+        if (n < lv && n < a.rp.n_rot && !a.rp.keys_prerotated) rotate_pair_direct(a.rp, ks[r], n, p);
       }
       __syncthreads();
     }

@@ -25,6 +25,7 @@ struct RopeParams {
   int gt, gh, gw;      // token grid
   int dt, dh, dw;      // channel widths of the t, h, w blocks
   int pair_mode;       // 0 interleaved, 1 half split
+  int keys_prerotated; // attention: keys arrive already rotated
   int n_rot;           // gt * gh * gw
   int base1, base2;    // first table entry of the h and w axes
   int n_entries;       // table entries: gt*dt/2 + gh*dh/2 + gw*dw/2

@@ -42,6 +42,7 @@ vidax_status make_rope(const vidax_rope3d_desc* r, int64_t max_tokens, int32_t d
   if ((int64_t)r->dim_t + r->dim_h + r->dim_w != d) return VIDAX_ERR_INVALID_ARG;
   if (!(r->theta > 0.0f) || !isfinite(r->theta)) return VIDAX_ERR_INVALID_ARG;
   if (r->pair_mode != 0 && r->pair_mode != 1) return VIDAX_ERR_INVALID_ARG;
+  if (r->keys_prerotated != 0 && r->keys_prerotated != 1) return VIDAX_ERR_INVALID_ARG;
   const int64_t n_rot = (int64_t)r->grid_t * r->grid_h * r->grid_w;
   if (n_rot > max_tokens) return VIDAX_ERR_INVALID_ARG;
   const int64_t entries = (int64_t)r->grid_t * (r->dim_t / 2) + (int64_t)r->grid_h * (r->dim_h / 2) +
@@ -55,6 +56,7 @@ vidax_status make_rope(const vidax_rope3d_desc* r, int64_t max_tokens, int32_t d
   out->dh = r->dim_h;
   out->dw = r->dim_w;
   out->pair_mode = r->pair_mode;
+  out->keys_prerotated = r->keys_prerotated;
   out->n_rot = (int)n_rot;
   out->base1 = r->grid_t * (r->dim_t / 2);
   out->base2 = out->base1 + r->grid_h * (r->dim_h / 2);
@@ -126,8 +128,10 @@ vidax_status vidax_rope3d(const void* x, void* y, int32_t B, int32_t L, int32_t 
   if (!aligned(x, 16) || !aligned(y, 16)) return VIDAX_ERR_INVALID_ARG;
   if (d != vidax::kHeadDim) return VIDAX_ERR_UNSUPPORTED;
   if (x != y && overlaps(x, (uint64_t)n * 2, y, (uint64_t)n * 2)) return VIDAX_ERR_INVALID_ARG;
+  vidax_rope3d_desc r = *rope;
+  r.keys_prerotated = 0;  // attention-only field
   RopeParams rp;
-  const vidax_status st = make_rope(rope, L, d, &rp);
+  const vidax_status st = make_rope(&r, L, d, &rp);
   if (st != VIDAX_OK) return st;
   if (B == 0 || L == 0 || H == 0) return VIDAX_OK;
   const hipError_t e = vidax::launch_rope3d((const uint16_t*)x, (uint16_t*)y, B, L, H, rp, stream);

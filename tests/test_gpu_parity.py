@@ -162,6 +162,27 @@ def test_naive_kernel_agrees(w):
     _full_case(w, impl=vx.attn_fwd_naive)
 
 
+@pytest.mark.parametrize("w", [inputs.WORKLOADS["tiny"], RAGGED[0], RAGGED[5]], ids=lambda w: w.name)
+def test_prerotated_keys(w):
+    """vidax_rope3d on k, then attention rotating only q: same result as the
+    fused rotation of both, against the oracle."""
+    import dataclasses
+
+    import torch
+
+    q, k, v, lv = inputs.make_qkv(w)
+    log(f"case prerotated keys {w.name}")
+    r = rope_of(w)
+    kd = to_dev(k)
+    krot = vx.rope3d(kd, r)
+    o, l = vx.attn_fwd(to_dev(q), krot, to_dev(v), scale=w.scale, kv_valid_len=lengths_dev(lv),
+                       rope=dataclasses.replace(r, keys_prerotated=True), return_lse=True)
+    torch.cuda.synchronize()
+    ro, rl = _oracle_full(w, q, k, v, lv)
+    assert_parity(to_bits(o), ro, f"{w.name} prerotated")
+    assert_lse(l.cpu().numpy(), rl, f"{w.name} prerotated")
+
+
 def test_zero_and_single_valid_keys():
     import torch
 
@@ -291,6 +312,25 @@ def _convex_bounds_ok(ob, v, lv, heads):
         if not (np.all(g >= lo - slack) and np.all(g <= hi + slack)):
             return False
     return True
+
+
+def test_full_size_prerotated_wan13b_sampled():
+    import dataclasses
+
+    import torch
+
+    w = inputs.WORKLOADS["wan13b_480p"]
+    q, k, v, lv = inputs.make_qkv(w)
+    log("case full-size wan13b_480p, keys rotated by vidax_rope3d")
+    r = rope_of(w)
+    krot = vx.rope3d(to_dev(k), r)
+    o = vx.attn_fwd(to_dev(q), krot, to_dev(v), scale=w.scale, rope=dataclasses.replace(r, keys_prerotated=True))
+    torch.cuda.synchronize()
+    ob = to_bits(o)
+    rows = _sample_rows(w.Lq, np.random.default_rng(w.seed + 100))
+    dec = oracle.bf16_bits_to_f64
+    ro, _ = oracle.attn_ref_rows(dec(q), dec(k), dec(v), w.scale, rows, rope=spec_of(w), workers=8)
+    assert_parity(ob[:, rows], ro, "wan13b_480p prerotated")
 
 
 @pytest.mark.parametrize("name,heads", [

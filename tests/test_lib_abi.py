@@ -25,7 +25,7 @@ def test_library_exports_every_declared_function():
     assert set(declared) == set(vx.EXPORTED_SYMBOLS), declared
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.vidax_abi_version() == 1
+    assert lib.vidax_abi_version() == 2
     for s, text in [(0, b"ok"), (1, b"invalid argument"), (2, b"unsupported configuration"), (3, b"kernel launch failed")]:
         assert lib.vidax_status_string(s) == text
     assert lib.vidax_status_string(99) == b"unknown status"
@@ -66,6 +66,9 @@ def test_attn_rejects_invalid_arguments(fn):
            vx.Rope((1, 8, 8), (44, 42, 42), theta=-1.0).desc(),
            vx.Rope((1, 8, 8), (44, 42, 42), pair_mode=2).desc(),
            vx.Rope((2, 8, 8), (44, 42, 42)).desc()]     # 128 rotated tokens > Lq = 64
+    flag = vx.Rope((1, 8, 8), (44, 42, 42)).desc()
+    flag.keys_prerotated = 2
+    bad.append(flag)
     for r in bad:
         assert _attn(fn, rope=r) == INV
     # rotary table larger than the on-chip table
