@@ -1,17 +1,21 @@
 #!/usr/bin/env python3
 """Benchmark of the video-attention hot path on one MI355X.
 
-One step = one call of vidax_attn_fwd (3D rotation fused into the Q/K loads,
-non-causal softmax attention, bf16 in/out, fp32 accumulation) on the
-Wan2.1-1.3B-shaped 832x480, 81-frame self-attention workload: B=1, H=12,
-d=128, token grid 21x30x52 -> L=32760, seeded synthetic N(0,1) inputs with
+One step = the whole hot path on one batch: vidax_rope3d rotates K (3D RoPE
+over the 21x30x52 token grid), then vidax_attn_fwd rotates Q as it loads it
+and computes non-causal softmax attention against the rotated K and V (bf16
+in/out, fp32 accumulation).  Workload: Wan2.1-1.3B-shaped 832x480, 81-frame
+self-attention, B=1, H=12, d=128, L=32760, seeded synthetic N(0,1) inputs with
 per-head RMS-normalised Q/K, inputs resident in HBM before timing starts.
+The variant that rotates both Q and K inside the attention kernel is timed
+beside it (``alt.fused_rope``).
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--all]
 
 Prints ONE JSON line on stdout (everything else goes to stderr).  FLOPs per
-call = 4 * B * H * Lq * Lv * d (valid keys only; exponentials, rotation and
-masking not counted).
+step = 4 * B * H * Lq * Lv * d (valid keys only; exponentials, rotation and
+masking not counted).  The roofline entry is the attention kernel alone,
+timed with HIP events on the stream it is launched on.
 """
 
 from __future__ import annotations
@@ -71,7 +75,11 @@ def traffic_from_counters(workload):
     return rec.get("hbm_bytes_per_launch")
 
 
-def time_gpu(w, steps, warmup):
+def time_gpu(w, steps, warmup, fused=False):
+    """Times `steps` steps.  Events bracket the attention launch of each step
+    (on the stream it runs on); the wall clock covers the whole step."""
+    import dataclasses
+
     import torch
 
     import paper_2609_18077_amd as vx
@@ -89,25 +97,39 @@ def time_gpu(w, steps, warmup):
     rope = vx.Rope(w.grid, w.dims, w.theta) if w.grid is not None else None
     o = torch.empty_like(qd)
     stream = torch.cuda.current_stream()
+    two_pass = rope is not None and not fused
+    if two_pass:
+        kr = torch.empty_like(kd)
+        rope_q = dataclasses.replace(rope, keys_prerotated=True)
 
-    def call():
-        vx.attn_fwd(qd, kd, vd, scale=w.scale, kv_valid_len=ld, rope=rope, out=o)
+    def prologue():
+        if two_pass:
+            vx.rope3d(kd, rope, out=kr, stream=stream)
+
+    def attention():
+        if two_pass:
+            vx.attn_fwd(qd, kr, vd, scale=w.scale, kv_valid_len=ld, rope=rope_q, out=o, stream=stream)
+        else:
+            vx.attn_fwd(qd, kd, vd, scale=w.scale, kv_valid_len=ld, rope=rope, out=o, stream=stream)
 
     for _ in range(warmup):
-        call()
+        prologue()
+        attention()
     torch.cuda.synchronize()
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(steps):
+        prologue()
         starts[i].record(stream)
-        call()
+        attention()
         ends[i].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    per = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])  # ms per launch
+    per = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])  # ms per attention launch
     return {
+        "two_pass": two_pass,
         "wall_ms_per_step": wall * 1e3 / steps,
         "event_ms_mean": float(per.mean()),
         "event_ms_median": float(np.median(per)),
@@ -196,6 +218,17 @@ def main():
     log(f"[bench] {w.name}: {r['event_ms_mean']:.3f} ms/launch (events), {r['wall_ms_per_step']:.3f} ms/step (wall), "
         f"{achieved:.1f} TFLOP/s = {100 * achieved / PEAK_BF16_TFLOPS:.1f}% of bf16 peak")
 
+    alt = None
+    if r["two_pass"]:
+        rf = time_gpu(w, max(5, args.steps // 2), 3, fused=True)
+        rf.pop("inputs")
+        alt = {"fused_rope": {
+            "ms_per_step": round(rf["wall_ms_per_step"], 4),
+            "tflops": round(fl / (rf["wall_ms_per_step"] * 1e-3) / 1e12, 2),
+            "what": "Q and K both rotated inside vidax_attn_fwd (no separate vidax_rope3d pass)"}}
+        log(f"[bench] fused-rope variant: {rf['wall_ms_per_step']:.3f} ms/step")
+        torch.cuda.empty_cache()
+
     extra = {}
     if args.all:
         rows = {}
@@ -205,7 +238,7 @@ def main():
             f2 = flops(ww, lvw)
             t = rr["event_ms_mean"] * 1e-3
             rows[name] = {
-                "ms": rr["event_ms_mean"], "ms_median": rr["event_ms_median"], "ms_min": rr["event_ms_min"],
+                "step_ms": rr["wall_ms_per_step"], "ms": rr["event_ms_mean"], "ms_median": rr["event_ms_median"], "ms_min": rr["event_ms_min"],
                 "tflops": f2 / t / 1e12, "pct_bf16_peak": 100 * f2 / t / 1e12 / PEAK_BF16_TFLOPS,
                 "algorithmic_GBs": algorithmic_bytes(ww, lvw) / t / 1e9,
                 "kv_valid_len": None if lvw is None else [int(x) for x in lvw],
@@ -243,7 +276,8 @@ def main():
             "workload": w.name,
             "B": w.B, "H": w.H, "Lq": w.Lq, "Lk": w.Lk, "d": w.d,
             "grid": list(w.grid) if w.grid else None,
-            "rope": "3d interleaved 44/42/42 theta=1e4, fused" if w.grid else None,
+            "rope": ("3d interleaved 44/42/42 theta=1e4: K by vidax_rope3d, Q inside vidax_attn_fwd"
+                     if r["two_pass"] else "3d interleaved 44/42/42 theta=1e4, fused") if w.grid else None,
             "kv_valid_len": None if lv is None else [int(x) for x in lv],
             "inputs": "N(0,1) bf16, per-head RMS-normalised Q/K" if w.rms_norm_qk else "N(0,1) bf16",
             "flops_per_call": fl,
@@ -255,8 +289,10 @@ def main():
             "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
             "traffic": traffic,
+            "kernel": "attn_fwd_kernel",
             "kernel_ms_mean": round(r["event_ms_mean"], 4),
         },
+        "alt": alt,
         "cpu_baseline": None if cpu is None else {k2: cpu[k2] for k2 in ("value", "unit", "cores", "kind", "sample")},
     }
     if extra:
