@@ -48,6 +48,8 @@
 // read and every staging write touches each bank at most the minimum number
 // of times, while operand offsets stay affine in the step index; rotary table
 // <= 32 KB.
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace vidax {
@@ -166,27 +168,35 @@ __device__ __forceinline__ uint32_t packed_pos(const AttnArgs& a, int n) {
   return ((uint32_t)t << 22) | ((uint32_t)h << 11) | (uint32_t)(rem - h * a.rp.gw);
 }
 
-// Element offset of 16-byte chunk c of row r of a K tile / V tile.  K rows of
-// 136 elements put row r's chunk c in 16-byte bank slot (r + c) mod 16; V rows
-// of 160 elements put it in slot (4 r + c) mod 16.
-constexpr int KROW = D + 8;
-constexpr int VROW = D + 32;
-constexpr int KTILE = BN * KROW;
-constexpr int VTILE = BN * VROW;
-__device__ __forceinline__ int k_off(int r, int c) { return r * KROW + (c << 3); }
-__device__ __forceinline__ int v_off(int r, int c) { return r * VROW + (c << 3); }
+// K and V tiles sit in LDS in MFMA operand order: 16 blocks of 1 KB, each
+// holding exactly what one wave reads for one matrix instruction, lane by lane.
+//   K block 2 st + blk: lane l's 16 bytes = key row 32 blk + (l & 31),
+//     d = 16 st + 8 (l >> 5) .. + 7 (A operand of S^T = K Q^T, d-step st).
+//   V block 4 ks + mb, half r (512 bytes): lane l's 8 bytes = key row
+//     16 ks + 8 r + 4 (l >> 5) + ((l & 15) >> 2), d = 32 mb + 16 ((l >> 4) & 1)
+//     + 4 (l & 3) .. + 3 (what the transposing read of lane l fetches for the
+//     V^T operand of d block mb, keys 16 ks .. 16 ks + 15).
+// Every operand read is one contiguous, bank-conflict-free 1 KB (K) or 512 B
+// (V) access at an offset that is a constant of the instruction, and each
+// block is filled by one direct 1 KB global -> LDS copy.
+constexpr int TILE = BN * D;  // elements per K or V tile
+constexpr int BLK = 512;      // elements per operand block
+
+typedef __attribute__((address_space(3))) void* lds_ptr;
 
 // ROPE: rotate the queries (and build the table); ROPE_K: also rotate the keys
 // while staging them (false when the caller passes pre-rotated keys).
 template <bool ROPE, bool ROPE_K>
 __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KTILE];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[2][VTILE];
+  // Two K and two V buffers, each its own LDS object so that the compiler can
+  // tell the direct copies into one buffer from the operand reads of another
+  // (and does not wait for the copies before those reads).
+  __shared__ __attribute__((aligned(16))) uint16_t K0[TILE], K1[TILE], V0[TILE], V1[TILE];
   __shared__ float2 tab[ROPE ? kAttnTableMax : 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31;
   const int hi = lane >> 5;
 
@@ -254,12 +264,24 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
     }
   }
 
-  // ---- staging: thread owns chunk kc of rows kr0 and kr0 + 32 of every K and V tile
-  const int kc = lane & 15;
-  const int kr0 = (lane >> 4) + 4 * wave;
-  const int goff[2] = {(kr0 * tok + kc * 8) * 2, ((kr0 + 32) * tok + kc * 8) * 2};  // bytes from the tile's first row
+  // ---- staging: wave w fills K blocks 2w, 2w + 1 (d-step w, both key blocks)
+  // and V blocks 2w, 2w + 1 of every tile.  Byte offsets from the tile's
+  // first row of what lane `lane` copies:
+  const int rbytes = tok * 2;  // bytes between consecutive tokens
+  const int kr0 = l32;                 // K rows kr0 and kr0 + 32 ...
+  const int kc = 2 * wave + hi;        // ... 16-byte chunk kc
+  const int kg0 = kr0 * rbytes + kc * 16;
+  const int kg1 = kg0 + 32 * rbytes;
+  int vg0, vg1;
+  {
+    const int vrow = 8 * hi + 4 * ((lane >> 4) & 1) + ((lane & 7) >> 1);
+    const int vd = 16 * ((lane >> 3) & 1) + 8 * (lane & 1);
+    const int b0 = 2 * wave, b1 = 2 * wave + 1;  // blocks (ks, mb) = (b >> 2, b & 3)
+    vg0 = (vrow + 16 * (b0 >> 2)) * rbytes + 2 * (vd + 32 * (b0 & 3));
+    vg1 = (vrow + 16 * (b1 >> 2)) * rbytes + 2 * (vd + 32 * (b1 & 3));
+  }
 
-  // rotary state of the two K rows (token index kr0 + 32 r + BN * tile)
+  // rotary state of the fused path: the thread owns chunk kc of K rows kr0, kr0 + 32
   PairIdx kpi[4];
   uint32_t kpos[2] = {0u, 0u};
   if (ROPE_K) {
@@ -277,16 +299,30 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
 
   const int ntiles = (lv + BN - 1) / BN;
 
-  // Rows of tile `tile` at or beyond lv lie outside the buffer's records and
-  // read as zero; tiles past the end read all zeros and are never used.
-  auto load_rows = [&](const uint16_t* base, int tile, uint4 reg[2]) {
+  // Buffer resource of tile `tile`: its records end at the last valid key, so
+  // rows at or beyond lv read as zero (and land in LDS as zero); tiles past
+  // the end read all zeros and are never used.
+  auto tile_rsrc = [&](const uint16_t* base, int tile) {
     const int rows = min(max(lv - tile * BN, 0), BN);
-    const int nbytes = __builtin_amdgcn_readfirstlane(rows * tok * 2);  // uniform
-    const __amdgpu_buffer_rsrc_t rs =
-        __builtin_amdgcn_make_buffer_rsrc((void*)(base + (size_t)tile * BN * tok), (short)0, nbytes, kBufferFlags);
+    const int nbytes = __builtin_amdgcn_readfirstlane(rows * rbytes);  // uniform
+    return __builtin_amdgcn_make_buffer_rsrc((void*)(base + (size_t)tile * BN * tok), (short)0, nbytes, kBufferFlags);
+  };
+
+  // Direct global -> LDS copy of the wave's two operand blocks of a tile (16
+  // bytes a lane, landing at the block base + 16 * lane).
+  auto dma_tile = [&](const uint16_t* base, int tile, uint16_t* buf, int g0, int g1) {
+    const __amdgpu_buffer_rsrc_t rs = tile_rsrc(base, tile);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)(buf + (2 * wave) * BLK), 16, g0, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)(buf + (2 * wave + 1) * BLK), 16, g1, 0, 0, 0);
+  };
+
+  // fused path: the thread's two K chunks through registers
+  auto load_k = [&](int tile, uint4 reg[2]) {
+    const __amdgpu_buffer_rsrc_t rs = tile_rsrc(kbh, tile);
+    const int g[2] = {kg0, kg1};
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
-      const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(rs, goff[r], 0, 0);
+      const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(rs, g[r], 0, 0);
       reg[r] = make_uint4(x[0], x[1], x[2], x[3]);
     }
   };
@@ -312,29 +348,17 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
       uint4 kv = reg[r];
-      if (ROPE_K) {
-        kv.x = rotate_pair(kv.x, cs[r][0]);
-        kv.y = rotate_pair(kv.y, cs[r][1]);
-        kv.z = rotate_pair(kv.z, cs[r][2]);
-        kv.w = rotate_pair(kv.w, cs[r][3]);
-      }
-      *reinterpret_cast<uint4*>(buf + k_off(kr0 + 32 * r, kc)) = kv;
+      kv.x = rotate_pair(kv.x, cs[r][0]);
+      kv.y = rotate_pair(kv.y, cs[r][1]);
+      kv.z = rotate_pair(kv.z, cs[r][2]);
+      kv.w = rotate_pair(kv.w, cs[r][3]);
+      *reinterpret_cast<uint4*>(buf + (2 * wave + r) * BLK + lane * 8) = kv;
     }
   };
 
-  auto store_v = [&](uint16_t* buf, const uint4 reg[2]) {
-#pragma unroll
-    for (int r = 0; r < 2; ++r) *reinterpret_cast<uint4*>(buf + v_off(kr0 + 32 * r, kc)) = reg[r];
-  };
-
-  // per-lane LDS element offsets of the MFMA operands
-  const int koff = k_off(l32, hi);  // + 16 st for d-step st, + 32 KROW for key block 1
-  // V^T via transposing reads: lane (h, g, i) = (hi, (lane >> 4) & 1, lane & 15)
-  // reads 4 d-values of key row 16 ks + 8 r + 4 h + i/4 at d = 32 mb + 16 g + 4 (i & 3).
-  const int vi = lane & 15;
-  const int vg = (lane >> 4) & 1;
-  const int vrow = 4 * hi + (vi >> 2);
-  const int voff = v_off(vrow, 2 * vg + ((vi & 3) >> 1)) + 4 * (vi & 1);  // + 32 mb for d block mb
+  // per-lane LDS element offsets of the MFMA operands (operand order, above)
+  const int koff = lane * 8;
+  const int voff = lane * 4;
 
   auto qk = [&](const uint16_t* kb, f32x16 s[2]) {
     s[0] = f32x16{};
@@ -343,7 +367,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
     for (int st = 0; st < 8; ++st) {
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk) {
-        const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kb + koff + 16 * st + blk * 32 * KROW);
+        const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kb + (2 * st + blk) * BLK + koff);
         s[blk] = mfma32(kop, qreg[st], s[blk]);
       }
     }
@@ -357,17 +381,18 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   const float c2 = a.c2;
   const uint32_t ones = 0x3f803f80u;  // bf16 (1, 1)
 
-  // p = exp2(s c - mref) as bf16 MFMA operands; returns this lane's sum of p
-  auto softmax_p = [&](const f32x16 s[2], bf16x8 pop[4]) {
+  // p = exp2(s c - mref) for the 32 keys of one key block as two bf16 MFMA
+  // operands (16 keys each); returns this lane's sum of p
+  auto softmax_p = [&](const f32x16& s, bf16x8 pop[2]) {
     const float nm = -mref;
     float tsum = 0.f;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
+    for (int ks = 0; ks < 2; ++ks) {
       uint32_t pw[4];
 #pragma unroll
       for (int e = 0; e < 8; e += 2) {
-        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[ks >> 1][8 * (ks & 1) + e], c2, nm));
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[ks >> 1][8 * (ks & 1) + e + 1], c2, nm));
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[8 * ks + e], c2, nm));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[8 * ks + e + 1], c2, nm));
         pw[e >> 1] = pack_bf16x2(p0, p1);
         tsum = dot2(pw[e >> 1], ones, tsum);
       }
@@ -376,19 +401,17 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
     return tsum;
   };
 
-  // probabilities of a score tile; resets the reference when a row's sum
-  // leaves [0, 2^64) (see the header)
-  auto softmax_tile = [&](const f32x16 s[2], bf16x8 pop[4]) {
+  // Probabilities of one key block.  A block whose row sum of p leaves
+  // [0, 2^64) resets the reference to the running max, rescaling the output
+  // (which may already hold the other block of the same tile, computed with
+  // the old reference) and the sum (see the header).
+  auto softmax_blk = [&](const f32x16& s, bf16x8 pop[2]) {
     float tsum = softmax_p(s, pop);
     if (__builtin_amdgcn_ballot_w64(!(tsum < kSumLimit)) != 0) {
-      float m0 = fmaxf(s[0][0], s[0][1]);
-      float m1 = fmaxf(s[1][0], s[1][1]);
+      float m = fmaxf(s[0], s[1]);
 #pragma unroll
-      for (int i = 2; i < 16; ++i) {
-        m0 = fmaxf(m0, s[0][i]);
-        m1 = fmaxf(m1, s[1][i]);
-      }
-      const float mnew = fmaxf(mref, wave_half_max(fmaxf(m0, m1)) * c2);
+      for (int i = 2; i < 16; ++i) m = fmaxf(m, s[i]);
+      const float mnew = fmaxf(mref, wave_half_max(m) * c2);
       const float alpha = __builtin_amdgcn_exp2f(mref - mnew);
       lsum *= alpha;
 #pragma unroll
@@ -401,62 +424,89 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
     lsum += tsum;
   };
 
-  auto pv = [&](const uint16_t* vb, const bf16x8 pop[4]) {
+  // O^T += V^T P^T over the 32 keys of key block `blk`
+  auto pv_blk = [&](const uint16_t* vb, const bf16x8 pop[2], int blk) {
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
+    for (int k2 = 0; k2 < 2; ++k2) {
+      const int ks = 2 * blk + k2;
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb) {
-        const i16x4 lo = lds_read_tr16(vb + voff + 32 * mb + (16 * ks) * VROW);
-        const i16x4 hi4 = lds_read_tr16(vb + voff + 32 * mb + (16 * ks + 8) * VROW);
+        const i16x4 lo = lds_read_tr16(vb + (4 * ks + mb) * BLK + voff);
+        const i16x4 hi4 = lds_read_tr16(vb + (4 * ks + mb) * BLK + BLK / 2 + voff);
         const bf16x8 vop = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
-        oacc[mb] = mfma32(vop, pop[ks], oacc[mb]);
+        oacc[mb] = mfma32(vop, pop[k2], oacc[mb]);
       }
     }
   };
 
-  // ---- prologue: K_0, V_0 and K_1 in LDS (both halves), scores of tile 0
-  {
-    uint4 k0[2], v0[2], k1[2];
+  // softmax and PV of one score tile, one key block at a time, so that the
+  // second block's softmax overlaps the first block's PV products
+  auto softmax_pv = [&](const f32x16 s[2], const uint16_t* vb) {
+    bf16x8 pop0[2], pop1[2];
+    softmax_blk(s[0], pop0);
+    pv_blk(vb, pop0, 0);
+    softmax_blk(s[1], pop1);
+    pv_blk(vb, pop1, 1);
+  };
+
+  // ---- prologue: K_0, V_0 and K_1 in LDS, scores of tile 0
+  if (ROPE_K) {
+    uint4 k0[2], k1[2];
     float2 cs0[2][4], cs1[2][4];
-    load_rows(kbh, 0, k0);
-    load_rows(vbh, 0, v0);
-    load_rows(kbh, 1, k1);
-    if (ROPE_K) {
-      fetch_coef(0, cs0);
-      fetch_coef(1, cs1);
-    }
-    store_k(Ks[0], k0, cs0);
-    store_v(Vs[0], v0);
-    store_k(Ks[1], k1, cs1);
+    load_k(0, k0);
+    load_k(1, k1);
+    fetch_coef(0, cs0);
+    fetch_coef(1, cs1);
+    store_k(K0, k0, cs0);
+    store_k(K1, k1, cs1);
+  } else {
+    dma_tile(kbh, 0, K0, kg0, kg1);
+    dma_tile(kbh, 1, K1, kg0, kg1);
   }
+  dma_tile(vbh, 0, V0, vg0, vg1);
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's copies have landed in LDS
   __syncthreads();
 
   f32x16 sa[2], sb[2];
-  qk(Ks[0], sa);
+  qk(K0, sa);
+  // step 0 refills K0 (K_2): every wave must be done reading K_0 first
+  __syncthreads();
 
-  auto step = [&](int j, f32x16 scur[2], f32x16 snext[2]) {
-    uint4 kn[2], vn[2];
+  // Step j (parity P = j & 1): scores of tile j + 1, softmax and PV of tile j,
+  // while K_{j+2} and V_{j+1} stream into the buffers that tiles j and j - 1
+  // have freed.  The buffers are chosen at compile time.
+  auto step = [&](auto parity, int j, f32x16 scur[2], f32x16 snext[2]) {
+    constexpr int P = decltype(parity)::value;
+    uint16_t* const kfree = P ? K1 : K0;  // held K_j
+    uint16_t* const knext = P ? K0 : K1;  // holds K_{j+1}
+    uint16_t* const vcur = P ? V1 : V0;   // holds V_j
+    uint16_t* const vfree = P ? V0 : V1;  // held V_{j-1}
+    uint4 kn[2];
     float2 cs[2][4];
-    load_rows(kbh, j + 2, kn);
-    load_rows(vbh, j + 1, vn);
-    if (ROPE_K) fetch_coef(j + 2, cs);
-    qk(Ks[(j + 1) & 1], snext);
-    bf16x8 pop[4];
-    softmax_tile(scur, pop);
-    pv(Vs[j & 1], pop);
-    store_k(Ks[j & 1], kn, cs);
-    store_v(Vs[(j + 1) & 1], vn);
+    if (ROPE_K) {
+      load_k(j + 2, kn);
+      fetch_coef(j + 2, cs);
+    } else {
+      dma_tile(kbh, j + 2, kfree, kg0, kg1);
+    }
+    dma_tile(vbh, j + 1, vfree, vg0, vg1);
+    qk(knext, snext);
+    softmax_pv(scur, vcur);
+    if (ROPE_K) store_k(kfree, kn, cs);
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's copies have landed
     __syncthreads();
   };
+  using even = std::integral_constant<int, 0>;
+  using odd = std::integral_constant<int, 1>;
 
   int j = 0;
   for (; j + 2 < ntiles; j += 2) {
-    step(j, sa, sb);
-    step(j + 1, sb, sa);
+    step(even(), j, sa, sb);
+    step(odd(), j + 1, sb, sa);
   }
   f32x16* slast = sa;
   if (j + 1 < ntiles) {
-    step(j, sa, sb);
+    step(even(), j, sa, sb);
     ++j;
     slast = sb;
   }
@@ -471,9 +521,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
           if (key >= lv) s[blk][i] = -INFINITY;
         }
     }
-    bf16x8 pop[4];
-    softmax_tile(s, pop);
-    pv(Vs[j & 1], pop);
+    softmax_pv(s, (j & 1) ? V1 : V0);
   }
 
   // ---- epilogue: O = O^T / l, lane holds query qrow, d = 32 mb + 8 g + 4 hi + (0..3)
