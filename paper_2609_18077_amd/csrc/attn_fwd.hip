@@ -1,15 +1,18 @@
 // Flash-attention forward for gfx950: bf16 MFMA (32x32x16) with fp32
-// accumulation, streaming softmax, fused 3D rotary embedding, per-batch
-// valid-key prefix.  Head dim 128.
+// accumulation, streaming softmax, 3D rotary embedding, per-batch valid-key
+// prefix.  Head dim 128.
 //
 // Work decomposition
 //   One workgroup = 8 waves = 256 query rows of one (batch, head); each wave
-//   owns 32 query rows.  Keys/values stream through LDS in tiles of 64, two
-//   buffers each.  The loop is software pipelined: while the softmax of tile j
-//   runs on the vector ALUs, the matrix cores already compute the scores of
-//   tile j+1; while the PV products of tile j run, the threads write the next
-//   K tile (rotated) and V tile into the free buffers.  One barrier per tile;
-//   the two waves sharing a SIMD overlap each other's matrix and vector work.
+//   owns 32 query rows, and the two waves sharing a SIMD overlap each other's
+//   matrix and vector work.  Keys/values stream through LDS in tiles of 64,
+//   two buffers each, one barrier per tile.  Step j is software pipelined:
+//   the matrix cores compute the scores of tile j + 1 while the vector ALUs
+//   turn the first key block (32 keys) of tile j into probabilities; the PV
+//   products of that block run while the second block's probabilities are
+//   computed; then the second block's PV products.  Meanwhile K_{j+2} and
+//   V_{j+1} are copied from global memory straight into LDS (buffer loads
+//   with the LDS flag: no registers, no LDS store instructions).
 //
 // Matrix-core formulation (per wave, per key tile)
 //   S^T[64 keys x 32 queries] = K_tile * Q^T   (16 MFMAs: 2 key blocks x 8 d-steps)
@@ -18,15 +21,15 @@
 //   softmax row max/sum are register-local plus one swap between the two lane
 //   halves, and the fp32 scores convert in place into the bf16 B operand of
 //   the PV product (no shuffles).  The key order inside a 16-key step is the
-//   accumulator's natural order.  V stays row-major in LDS; its V^T operands
-//   are read with the gfx950 transposing LDS load (ds_read_b64_tr_b16), which
-//   hands each lane 4 keys of one d column per read.
+//   accumulator's natural order.  The V^T operands come from the gfx950
+//   transposing LDS read (ds_read_b64_tr_b16), which hands each lane 4 keys
+//   of one d column per read.
 //
 // Softmax: p = exp2(s * c - m) with c = |scale| * log2 e in one FMA (the
 // rotated query is rounded to bf16 unscaled; a negative scale negates it, a
 // zero scale zeroes it).  The reference m of a row is not the running max but
-// the max of the tile that last reset it: no per-tile max is computed.  A
-// tile whose row sum of p reaches 2^64 (or is not finite -- the first tile
+// the max of the block that last reset it: no per-tile max is computed.  A key
+// block whose row sum of p reaches 2^64 (or is not finite -- the first block
 // always is, since m starts at -inf) resets m to the running max, rescales the
 // output and sum, and recomputes its p.  p therefore never exceeds 2^64, so
 // the bf16 P, fp32 sums and fp32 output accumulators cannot overflow, and the
@@ -35,19 +38,19 @@
 //
 // Rotary embedding: each workgroup builds an fp32 (cos, sin) table per (axis,
 // position, frequency) in LDS; each axis has one extra identity position used
-// by unrotated tokens.  A thread fetches the coefficients of the K rows it
-// will stage next at the start of a pipeline step, so the LDS latency of the
-// (scattered) table reads hides behind the matrix work, and rotates in fp32
-// when it writes the tile.
+// by unrotated tokens.  Queries are rotated as they are loaded.  Keys either
+// arrive rotated (rotated once by the standalone rotary kernel, which costs
+// less than rotating every key tile once per query tile) or are rotated here:
+// then K goes through registers instead of the direct copy, the coefficients
+// of the rows staged next are fetched at the start of a step, and the rotated
+// rows are written to LDS after the PV products.
 //
 // Global loads use buffer resources whose record count ends at the last valid
-// key, so rows past kv_valid_len read as zero without any per-lane test.
+// key, so rows past kv_valid_len read as zero (and land in LDS as zero)
+// without any per-lane test.
 //
-// LDS (per workgroup): K tiles 2 x 17 KB and V tiles 2 x 20 KB, row-major with
-// padded rows (K: 256 + 16 bytes, V: 256 + 64 bytes) so that every operand
-// read and every staging write touches each bank at most the minimum number
-// of times, while operand offsets stay affine in the step index; rotary table
-// <= 32 KB.
+// LDS (per workgroup): K and V tiles 2 x 16 KB each, stored in MFMA operand
+// order (see below); rotary table <= 32 KB.
 #include <type_traits>
 
 #include "common.hpp"
