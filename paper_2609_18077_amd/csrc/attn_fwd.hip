@@ -86,6 +86,7 @@ struct AttnArgs {
 };
 
 typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
@@ -184,13 +185,26 @@ __device__ __forceinline__ uint32_t packed_pos(const AttnArgs& a, int n) {
 // block is filled by one direct 1 KB global -> LDS copy.
 constexpr int TILE = BN * D;  // elements per K or V tile
 constexpr int BLK = 512;      // elements per operand block
+constexpr int kOutStores = 17;  // store instructions per wave for one tile's output (O and LSE)
+// s_waitcnt immediate: vmcnt <= kOutStores, expcnt and lgkmcnt not waited for
+constexpr int kWaitCopiesBehindStores = (kOutStores & 15) | (7 << 4) | (15 << 8) | ((kOutStores >> 4) << 14);
+#ifndef VIDAX_SHORT_KEYS
+#define VIDAX_SHORT_KEYS 2048
+#endif
+constexpr int kAttnShortKeys = VIDAX_SHORT_KEYS;  // Lk at or below which the persistent form is used
 
 typedef __attribute__((address_space(3))) void* lds_ptr;
 
 // ROPE: rotate the queries (and build the table); ROPE_K: also rotate the keys
 // while staging them (false when the caller passes pre-rotated keys).
-template <bool ROPE, bool ROPE_K>
+// PERSIST: one workgroup per CU loops over query tiles; the next tile's
+// queries are loaded while the current tile computes, and a finished tile's
+// output is stored after the next tile's K/V copies have been issued, so that
+// neither the query loads nor the output stores stall the pipeline (short key
+// sequences, where they are a large share of a tile's time).
+template <bool ROPE, bool ROPE_K, bool PERSIST>
 __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
+  static_assert(!(PERSIST && ROPE), "the persistent form serves unrotated attention");
   // Two K and two V buffers, each its own LDS object so that the compiler can
   // tell the direct copies into one buffer from the operand reads of another
   // (and does not wait for the copies before those reads).
@@ -202,62 +216,64 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31;
   const int hi = lane >> 5;
+  const int tok = a.H * D;     // elements between consecutive tokens
+  const int rbytes = tok * 2;  // bytes between consecutive tokens
 
-  // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
-  // contiguous range of logical tiles so the query tiles of one (b, h) share
-  // that XCD's L2 for the K/V stream.
-  int lid;
-  {
-    const int i = blockIdx.x, n = a.nwg;
-    const int per = n >> 3, rem = n & 7, xcd = i & 7, kk = i >> 3;
-    lid = xcd < rem ? xcd * (per + 1) + kk : rem * (per + 1) + (xcd - rem) * per + kk;
-  }
-  const int qt = lid % a.nqt;
-  const int bh = lid / a.nqt;
-  const int h = bh % a.H;
-  const int b = bh / a.H;
-
-  int lv = a.Lk;
-  if (a.kv_valid_len) lv = min(max(a.kv_valid_len[b], 0), a.Lk);
-  lv = __builtin_amdgcn_readfirstlane(lv);  // uniform: keeps buffer descriptors in SGPRs
-
-  const int tok = a.H * D;  // elements between consecutive tokens
-  const uint16_t* qbh = a.q + (size_t)b * a.Lq * tok + (size_t)h * D;
-  const uint16_t* kbh = a.k + (size_t)b * a.Lk * tok + (size_t)h * D;
-  const uint16_t* vbh = a.v + (size_t)b * a.Lk * tok + (size_t)h * D;
-  uint16_t* obh = a.o + (size_t)b * a.Lq * tok + (size_t)h * D;
-
-  const int qrow = qt * BM + wave * 32 + l32;
-  const bool qlive = qrow < a.Lq;
-
-  if (lv == 0) {
-    // no valid key: output 0, lse -inf
-    if (qlive) {
-#pragma unroll
-      for (int s = 0; s < 8; ++s)
-        *reinterpret_cast<uint4*>(obh + (size_t)qrow * tok + (2 * s + hi) * 8) = make_uint4(0, 0, 0, 0);
-      if (a.lse && hi == 0) a.lse[((size_t)b * a.H + h) * a.Lq + qrow] = -INFINITY;
+  // ---- state of the current query tile (logical tile lid: query tile
+  // lid % nqt of (b, h) = (lid / nqt / H, lid / nqt % H))
+  int b = 0, h = 0, qrow = 0, lv = 0, ntiles = 0;
+  bool qlive = false;
+  const uint16_t* kbh = a.k;
+  const uint16_t* vbh = a.v;
+  // Tile order: the query tiles of one (b, h) are consecutive (the K/V
+  // stream of that head is then shared in L2); the persistent form instead
+  // runs the heads of one query tile together, so that the rows its
+  // workgroups read and write at the same time are whole tokens of Q and O.
+  auto tile_of = [&](int lid, int& qt, int& bh) __attribute__((always_inline)) {
+    if (PERSIST) {
+      qt = lid / (a.B * a.H);
+      bh = lid - qt * (a.B * a.H);
+    } else {
+      qt = lid % a.nqt;
+      bh = lid / a.nqt;
     }
-    return;
-  }
+  };
+  auto begin_tile = [&](int lid) __attribute__((always_inline)) {
+    int qt, bh;
+    tile_of(lid, qt, bh);
+    h = bh % a.H;
+    b = bh / a.H;
+    int l = a.Lk;
+    if (a.kv_valid_len) l = min(max(a.kv_valid_len[b], 0), a.Lk);
+    lv = __builtin_amdgcn_readfirstlane(l);  // uniform: keeps buffer descriptors in SGPRs
+    kbh = a.k + (size_t)b * a.Lk * tok + (size_t)h * D;
+    vbh = a.v + (size_t)b * a.Lk * tok + (size_t)h * D;
+    qrow = qt * BM + wave * 32 + l32;
+    qlive = qrow < a.Lq;
+    ntiles = (lv + BN - 1) / BN;
+  };
 
-  if (ROPE) {
-    for (int e = tid; e < a.tentries; e += NT) tab[e] = attn_table_entry(a, e);
-    __syncthreads();
-  }
+  // raw query chunks 2s + hi (s = 0..7) of this lane's row of tile lid
+  auto load_q = [&](int lid, uint4 raw[8]) __attribute__((always_inline)) {
+    int qt, bh;
+    tile_of(lid, qt, bh);
+    const int row = qt * BM + wave * 32 + l32;
+    const uint16_t* qp = a.q + (size_t)(bh / a.H) * a.Lq * tok + (size_t)(bh % a.H) * D + (size_t)row * tok;
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+      raw[s] = row < a.Lq ? *reinterpret_cast<const uint4*>(qp + (2 * s + hi) * 8) : make_uint4(0, 0, 0, 0);
+  };
 
   // ---- Q: lane holds query qrow, d-chunks 2s + hi (s = 0..7) as MFMA B operands
   bf16x8 qreg[8];
-  {
+  auto make_q = [&](const uint4 raw[8]) __attribute__((always_inline)) {
     const uint32_t qpos = ROPE ? packed_pos(a, qlive ? qrow : a.rp.n_rot) : 0u;
     const uint32_t sgn = a.qsign < 0.f ? 0x80008000u : 0u;
     const uint32_t keep = a.qsign == 0.f ? 0u : 0xffffffffu;
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       const int c = 2 * s + hi;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (qlive) v = *reinterpret_cast<const uint4*>(qbh + (size_t)qrow * tok + c * 8);
-      uint32_t wq[4] = {v.x, v.y, v.z, v.w};
+      uint32_t wq[4] = {raw[s].x, raw[s].y, raw[s].z, raw[s].w};
 #pragma unroll
       for (int p = 0; p < 4; ++p) {
         if (ROPE) wq[p] = rotate_pair(wq[p], table_entry(tab, pair_idx(a, 4 * c + p), qpos));
@@ -265,12 +281,11 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
       }
       qreg[s] = __builtin_bit_cast(bf16x8, make_uint4(wq[0], wq[1], wq[2], wq[3]));
     }
-  }
+  };
 
   // ---- staging: wave w fills K blocks 2w, 2w + 1 (d-step w, both key blocks)
   // and V blocks 2w, 2w + 1 of every tile.  Byte offsets from the tile's
   // first row of what lane `lane` copies:
-  const int rbytes = tok * 2;  // bytes between consecutive tokens
   const int kr0 = l32;                 // K rows kr0 and kr0 + 32 ...
   const int kc = 2 * wave + hi;        // ... 16-byte chunk kc
   const int kg0 = kr0 * rbytes + kc * 16;
@@ -300,12 +315,10 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
     }
   }
 
-  const int ntiles = (lv + BN - 1) / BN;
-
   // Buffer resource of tile `tile`: its records end at the last valid key, so
   // rows at or beyond lv read as zero (and land in LDS as zero); tiles past
   // the end read all zeros and are never used.
-  auto tile_rsrc = [&](const uint16_t* base, int tile) {
+  auto tile_rsrc = [&](const uint16_t* base, int tile) __attribute__((always_inline)) {
     const int rows = min(max(lv - tile * BN, 0), BN);
     const int nbytes = __builtin_amdgcn_readfirstlane(rows * rbytes);  // uniform
     return __builtin_amdgcn_make_buffer_rsrc((void*)(base + (size_t)tile * BN * tok), (short)0, nbytes, kBufferFlags);
@@ -313,14 +326,14 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
 
   // Direct global -> LDS copy of the wave's two operand blocks of a tile (16
   // bytes a lane, landing at the block base + 16 * lane).
-  auto dma_tile = [&](const uint16_t* base, int tile, uint16_t* buf, int g0, int g1) {
+  auto dma_tile = [&](const uint16_t* base, int tile, uint16_t* buf, int g0, int g1) __attribute__((always_inline)) {
     const __amdgpu_buffer_rsrc_t rs = tile_rsrc(base, tile);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)(buf + (2 * wave) * BLK), 16, g0, 0, 0, 0);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)(buf + (2 * wave + 1) * BLK), 16, g1, 0, 0, 0);
   };
 
   // fused path: the thread's two K chunks through registers
-  auto load_k = [&](int tile, uint4 reg[2]) {
+  auto load_k = [&](int tile, uint4 reg[2]) __attribute__((always_inline)) {
     const __amdgpu_buffer_rsrc_t rs = tile_rsrc(kbh, tile);
     const int g[2] = {kg0, kg1};
 #pragma unroll
@@ -333,7 +346,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   // Coefficients for the two K rows of the next tile to be staged; advances
   // the rows' packed coordinates by BN tokens.  Rows at or past the rotated
   // prefix take the identity position.
-  auto fetch_coef = [&](int tile, float2 cs[2][4]) {
+  auto fetch_coef = [&](int tile, float2 cs[2][4]) __attribute__((always_inline)) {
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
       const uint32_t pos = tile * BN + kr0 + 32 * r < a.rp.n_rot ? kpos[r] : a.pos_sent;
@@ -347,7 +360,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
     }
   };
 
-  auto store_k = [&](uint16_t* buf, const uint4 reg[2], const float2 cs[2][4]) {
+  auto store_k = [&](uint16_t* buf, const uint4 reg[2], const float2 cs[2][4]) __attribute__((always_inline)) {
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
       uint4 kv = reg[r];
@@ -363,7 +376,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   const int koff = lane * 8;
   const int voff = lane * 4;
 
-  auto qk = [&](const uint16_t* kb, f32x16 s[2]) {
+  auto qk = [&](const uint16_t* kb, f32x16 s[2]) __attribute__((always_inline)) {
     s[0] = f32x16{};
     s[1] = f32x16{};
 #pragma unroll
@@ -377,16 +390,20 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   };
 
   f32x16 oacc[4];
-#pragma unroll
-  for (int mb = 0; mb < 4; ++mb) oacc[mb] = f32x16{};
   float mref = -INFINITY;  // reference max (log2 units), identical in both lane halves
   float lsum = 0.f;        // this lane half's partial sum of p
+  auto reset_acc = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) oacc[mb] = f32x16{};
+    mref = -INFINITY;
+    lsum = 0.f;
+  };
   const float c2 = a.c2;
   const uint32_t ones = 0x3f803f80u;  // bf16 (1, 1)
 
   // p = exp2(s c - mref) for the 32 keys of one key block as two bf16 MFMA
   // operands (16 keys each); returns this lane's sum of p
-  auto softmax_p = [&](const f32x16& s, bf16x8 pop[2]) {
+  auto softmax_p = [&](const f32x16& s, bf16x8 pop[2]) __attribute__((always_inline)) {
     const float nm = -mref;
     float tsum = 0.f;
 #pragma unroll
@@ -408,7 +425,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   // [0, 2^64) resets the reference to the running max, rescaling the output
   // (which may already hold the other block of the same tile, computed with
   // the old reference) and the sum (see the header).
-  auto softmax_blk = [&](const f32x16& s, bf16x8 pop[2]) {
+  auto softmax_blk = [&](const f32x16& s, bf16x8 pop[2]) __attribute__((always_inline)) {
     float tsum = softmax_p(s, pop);
     if (__builtin_amdgcn_ballot_w64(!(tsum < kSumLimit)) != 0) {
       float m = fmaxf(s[0], s[1]);
@@ -428,7 +445,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   };
 
   // O^T += V^T P^T over the 32 keys of key block `blk`
-  auto pv_blk = [&](const uint16_t* vb, const bf16x8 pop[2], int blk) {
+  auto pv_blk = [&](const uint16_t* vb, const bf16x8 pop[2], int blk) __attribute__((always_inline)) {
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) {
       const int ks = 2 * blk + k2;
@@ -444,7 +461,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
 
   // softmax and PV of one score tile, one key block at a time, so that the
   // second block's softmax overlaps the first block's PV products
-  auto softmax_pv = [&](const f32x16 s[2], const uint16_t* vb) {
+  auto softmax_pv = [&](const f32x16 s[2], const uint16_t* vb) __attribute__((always_inline)) {
     bf16x8 pop0[2], pop1[2];
     softmax_blk(s[0], pop0);
     pv_blk(vb, pop0, 0);
@@ -452,33 +469,30 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
     pv_blk(vb, pop1, 1);
   };
 
-  // ---- prologue: K_0, V_0 and K_1 in LDS, scores of tile 0
-  if (ROPE_K) {
-    uint4 k0[2], k1[2];
-    float2 cs0[2][4], cs1[2][4];
-    load_k(0, k0);
-    load_k(1, k1);
-    fetch_coef(0, cs0);
-    fetch_coef(1, cs1);
-    store_k(K0, k0, cs0);
-    store_k(K1, k1, cs1);
-  } else {
-    dma_tile(kbh, 0, K0, kg0, kg1);
-    dma_tile(kbh, 1, K1, kg0, kg1);
-  }
-  dma_tile(vbh, 0, V0, vg0, vg1);
-  __builtin_amdgcn_s_waitcnt(0);  // this wave's copies have landed in LDS
-  __syncthreads();
+  // K_0, K_1 and V_0 of the current tile into K0, K1, V0
+  auto first_copies = [&]() __attribute__((always_inline)) {
+    if (ROPE_K) {
+      uint4 k0[2], k1[2];
+      float2 cs0[2][4], cs1[2][4];
+      load_k(0, k0);
+      load_k(1, k1);
+      fetch_coef(0, cs0);
+      fetch_coef(1, cs1);
+      store_k(K0, k0, cs0);
+      store_k(K1, k1, cs1);
+    } else {
+      dma_tile(kbh, 0, K0, kg0, kg1);
+      dma_tile(kbh, 1, K1, kg0, kg1);
+    }
+    dma_tile(vbh, 0, V0, vg0, vg1);
+  };
 
   f32x16 sa[2], sb[2];
-  qk(K0, sa);
-  // step 0 refills K0 (K_2): every wave must be done reading K_0 first
-  __syncthreads();
 
   // Step j (parity P = j & 1): scores of tile j + 1, softmax and PV of tile j,
   // while K_{j+2} and V_{j+1} stream into the buffers that tiles j and j - 1
   // have freed.  The buffers are chosen at compile time.
-  auto step = [&](auto parity, int j, f32x16 scur[2], f32x16 snext[2]) {
+  auto step = [&](auto parity, int j, f32x16 scur[2], f32x16 snext[2]) __attribute__((always_inline)) {
     constexpr int P = decltype(parity)::value;
     uint16_t* const kfree = P ? K1 : K0;  // held K_j
     uint16_t* const knext = P ? K0 : K1;  // holds K_{j+1}
@@ -502,48 +516,145 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   using even = std::integral_constant<int, 0>;
   using odd = std::integral_constant<int, 1>;
 
-  int j = 0;
-  for (; j + 2 < ntiles; j += 2) {
-    step(even(), j, sa, sb);
-    step(odd(), j + 1, sb, sa);
-  }
-  f32x16* slast = sa;
-  if (j + 1 < ntiles) {
-    step(even(), j, sa, sb);
-    ++j;
-    slast = sb;
-  }
-  {
-    f32x16 s[2] = {slast[0], slast[1]};
-    if (j * BN + BN > lv) {
-#pragma unroll
-      for (int blk = 0; blk < 2; ++blk)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int key = j * BN + blk * 32 + 8 * (i >> 2) + 4 * hi + (i & 3);
-          if (key >= lv) s[blk][i] = -INFINITY;
-        }
+  // the tile whose first copies have landed (and been published): scores of
+  // tile 0, the pipelined steps, and the last tile's softmax and PV
+  auto run_tile = [&]() __attribute__((always_inline)) {
+    qk(K0, sa);
+    // step 0 refills K0 (with K_2): every wave must be done reading K_0 first
+    __syncthreads();
+    int j = 0;
+    for (; j + 2 < ntiles; j += 2) {
+      step(even(), j, sa, sb);
+      step(odd(), j + 1, sb, sa);
     }
-    softmax_pv(s, (j & 1) ? V1 : V0);
-  }
+    f32x16* slast = sa;
+    if (j + 1 < ntiles) {
+      step(even(), j, sa, sb);
+      ++j;
+      slast = sb;
+    }
+    {
+      f32x16 s[2] = {slast[0], slast[1]};
+      if (j * BN + BN > lv) {
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int key = j * BN + blk * 32 + 8 * (i >> 2) + 4 * hi + (i & 3);
+            if (key >= lv) s[blk][i] = -INFINITY;
+          }
+      }
+      softmax_pv(s, (j & 1) ? V1 : V0);
+    }
+  };
 
-  // ---- epilogue: O = O^T / l, lane holds query qrow, d = 32 mb + 8 g + 4 hi + (0..3)
-  const float l = wave_half_sum(lsum);
-  const float inv = 1.0f / l;
-  if (qlive) {
-    uint16_t* orow = obh + (size_t)qrow * tok;
+  // ---- output: O = O^T / l (zero when no key is valid), LSE = m + ln l.
+  // Lane holds query qrow, d = 32 mb + 8 g + 4 hi + (0..3).  Buffer stores:
+  // lanes without a row address past the records and are dropped, so every
+  // wave issues exactly kOutStores store instructions.
+  auto store_o = [&](int ob, int oh, int orow, bool olive, bool empty) __attribute__((always_inline)) {
+    const float l = wave_half_sum(lsum);
+    const float inv = empty ? 0.f : 1.0f / l;
+    const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(a.o + (size_t)ob * a.Lq * tok), (short)0, a.Lq * rbytes, kBufferFlags);
+    const int obase = olive ? (orow * tok + oh * D) * 2 : 0x7ffffff0;
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int d = mb * 32 + 8 * g + 4 * hi;
-        uint2 pk;
-        pk.x = pack_bf16x2(oacc[mb][4 * g + 0] * inv, oacc[mb][4 * g + 1] * inv);
-        pk.y = pack_bf16x2(oacc[mb][4 * g + 2] * inv, oacc[mb][4 * g + 3] * inv);
-        *reinterpret_cast<uint2*>(orow + d) = pk;
+        u32x2 pk;
+        pk[0] = pack_bf16x2(oacc[mb][4 * g + 0] * inv, oacc[mb][4 * g + 1] * inv);
+        pk[1] = pack_bf16x2(oacc[mb][4 * g + 2] * inv, oacc[mb][4 * g + 3] * inv);
+        __builtin_amdgcn_raw_buffer_store_b64(pk, ro, olive ? obase + d * 2 : obase, 0, 0);
       }
-    if (a.lse && hi == 0)
-      a.lse[((size_t)b * a.H + h) * a.Lq + qrow] = (mref + __log2f(l)) * 0.69314718055994531f;
+    const __amdgpu_buffer_rsrc_t rl = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(a.lse ? a.lse + ((size_t)ob * a.H + oh) * a.Lq : a.lse), (short)0, a.lse ? a.Lq * 4 : 0,
+        kBufferFlags);
+    const float lse = empty ? -INFINITY : (mref + __log2f(l)) * 0.69314718055994531f;
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(lse), rl, olive && hi == 0 ? orow * 4 : 0x7ffffff0, 0, 0);
+  };
+
+  if constexpr (!PERSIST) {
+    // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
+    // contiguous range of logical tiles so the query tiles of one (b, h)
+    // share that XCD's L2 for the K/V stream.
+    int lid;
+    {
+      const int i = blockIdx.x, n = a.nwg;
+      const int per = n >> 3, rem = n & 7, xcd = i & 7, kk = i >> 3;
+      lid = xcd < rem ? xcd * (per + 1) + kk : rem * (per + 1) + (xcd - rem) * per + kk;
+    }
+    begin_tile(lid);
+    reset_acc();
+    if (lv == 0) {  // no valid key: O = 0, LSE = -inf
+      store_o(b, h, qrow, qlive, true);
+      return;
+    }
+    if (ROPE) {
+      for (int e = tid; e < a.tentries; e += NT) tab[e] = attn_table_entry(a, e);
+      __syncthreads();
+    }
+    {
+      uint4 raw[8];
+      load_q(lid, raw);
+      make_q(raw);
+    }
+    first_copies();
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's copies have landed in LDS
+    __syncthreads();
+    run_tile();
+    store_o(b, h, qrow, qlive, false);
+  } else {
+    // XCD x owns a contiguous range of logical tiles; its workgroups stride
+    // through it together, so the heads of a query tile run at the same time.
+    int lid, it_end, it_step;
+    {
+      const int i = blockIdx.x, n = a.nwg;
+      const int per = n >> 3, rem = n & 7, xcd = i & 7, kk = i >> 3;
+      const int start = xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per;
+      lid = start + kk;
+      it_end = start + per + (xcd < rem ? 1 : 0);
+      it_step = (int)(gridDim.x >> 3);  // the grid is a multiple of 8
+    }
+    if (lid >= it_end) return;
+    uint4 raw[8];
+    begin_tile(lid);
+    load_q(lid, raw);
+    if (lv > 0) first_copies();
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    while (true) {
+      const int next = lid + it_step;
+      const bool has_next = next < it_end;
+      const bool empty = lv == 0;
+      reset_acc();
+      if (!empty) {
+        make_q(raw);
+        // the next tile's queries load while this tile computes (the first
+        // step's wait for its copies also covers these older loads)
+        if (has_next) load_q(next, raw);
+        run_tile();
+      } else if (has_next) {
+        load_q(next, raw);
+      }
+      // every wave is done with this tile's LDS; start the next tile's
+      // copies, then store this tile's output behind them
+      __syncthreads();
+      const int ob = b, oh = h, orow = qrow;
+      const bool olive = qlive;
+      if (has_next) {
+        begin_tile(next);
+        if (lv > 0) first_copies();
+      }
+      store_o(ob, oh, orow, olive, empty);
+      if (!has_next) break;
+      // vector memory operations complete in issue order: waiting until only
+      // the output stores are outstanding means the copies have landed
+      __builtin_amdgcn_s_waitcnt(kWaitCopiesBehindStores);
+      __syncthreads();
+      lid = next;
+    }
   }
 }
 
@@ -555,6 +666,19 @@ bool attn_rope_supported(const RopeParams& rp) {
   if (rp.gw > kAttnGridHWMax || rp.gh > kAttnGridHWMax || rp.gt > kAttnGridTMax) return false;
   const long entries = (long)(rp.gt + 1) * (rp.dt / 2) + (long)(rp.gh + 1) * (rp.dh / 2) + (long)(rp.gw + 1) * (rp.dw / 2);
   return entries <= kAttnTableMax;
+}
+
+// Compute units of the current device (queried once per device).
+static int cu_count() {
+  static int counts[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (counts[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    counts[dev] = n;
+  }
+  return counts[dev];
 }
 
 hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o,
@@ -580,12 +704,18 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
     a.pos_step = (st << 22) | (sh << 11) | sw;
     a.pos_sent = ((uint32_t)rp.gt << 22) | ((uint32_t)rp.gh << 11) | (uint32_t)rp.gw;
   }
+  // short key sequences without rotation: one persistent workgroup per CU
+  const int cus = cu_count();
+  const bool persist = !rp.enabled && Lk <= kAttnShortKeys && nwg > 4L * cus;
   if (rp.enabled && !rp.keys_prerotated)
-    hipLaunchKernelGGL((attn_fwd_kernel<true, true>), dim3((unsigned)nwg), dim3(NT), 0, stream, a);
+    hipLaunchKernelGGL((attn_fwd_kernel<true, true, false>), dim3((unsigned)nwg), dim3(NT), 0, stream, a);
   else if (rp.enabled)
-    hipLaunchKernelGGL((attn_fwd_kernel<true, false>), dim3((unsigned)nwg), dim3(NT), 0, stream, a);
+    hipLaunchKernelGGL((attn_fwd_kernel<true, false, false>), dim3((unsigned)nwg), dim3(NT), 0, stream, a);
+  else if (persist)
+    hipLaunchKernelGGL((attn_fwd_kernel<false, false, true>), dim3((unsigned)(8 * ((cus + 7) / 8))), dim3(NT), 0,
+                       stream, a);
   else
-    hipLaunchKernelGGL((attn_fwd_kernel<false, false>), dim3((unsigned)nwg), dim3(NT), 0, stream, a);
+    hipLaunchKernelGGL((attn_fwd_kernel<false, false, false>), dim3((unsigned)nwg), dim3(NT), 0, stream, a);
   return hipGetLastError();
 }
 

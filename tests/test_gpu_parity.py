@@ -300,10 +300,15 @@ def _sample_rows(L, rng, n=160):
 
 def _convex_bounds_ok(ob, v, lv, heads):
     """Every output component lies in [min, max] of the valid value rows (per
-    batch, head, channel), up to one bf16 rounding of the output."""
+    batch, head, channel), up to one bf16 rounding of the output; a batch
+    without valid keys has an all-zero output."""
     got = oracle.bf16_bits_to_f64(ob)
     for b in range(ob.shape[0]):
         n = v.shape[1] if lv is None else int(np.clip(lv[b], 0, v.shape[1]))
+        if n == 0:
+            if np.any(got[b][:, heads] != 0):
+                return False
+            continue
         vv = oracle.bf16_bits_to_f64(v[b, :n][:, heads])  # [n, Hs, d]
         lo = vv.min(axis=0)
         hi = vv.max(axis=0)
@@ -312,6 +317,32 @@ def _convex_bounds_ok(ob, v, lv, heads):
         if not (np.all(g >= lo - slack) and np.all(g <= hi + slack)):
             return False
     return True
+
+
+# Short key sequences without rotation at more than four query tiles per CU
+# run as one persistent workgroup per CU looping over tiles: empty batches
+# (Lv = 0), a ragged last query tile, Lk at the persistent-form limit.
+PERSISTENT = [
+    inputs.custom("persist_empty_batch", B=2, H=8, Lq=20000, Lk=300, seed=31, kv_valid=("fixed", [0, 173])),
+    inputs.custom("persist_long_keys", B=1, H=16, Lq=17000, Lk=2048, seed=32),
+]
+
+
+@pytest.mark.parametrize("w", PERSISTENT, ids=lambda w: w.name)
+def test_persistent_short_keys_sampled(w):
+    import torch
+
+    q, k, v, lv = inputs.make_qkv(w)
+    log(f"case persistent form {w.name}")
+    o, l = vx.attn_fwd(to_dev(q), to_dev(k), to_dev(v), scale=w.scale, kv_valid_len=lengths_dev(lv), return_lse=True)
+    torch.cuda.synchronize()
+    ob, lse = to_bits(o), l.cpu().numpy()
+    rows = _sample_rows(w.Lq, np.random.default_rng(w.seed + 100))
+    dec = oracle.bf16_bits_to_f64
+    ro, rl = oracle.attn_ref_rows(dec(q), dec(k), dec(v), w.scale, rows, kv_valid_len=lv, workers=8)
+    assert_parity(ob[:, rows], ro, w.name)
+    assert_lse(lse[:, :, rows], rl, w.name)
+    assert _convex_bounds_ok(ob, v, lv, list(range(w.H)))
 
 
 def test_full_size_prerotated_wan13b_sampled():
