@@ -13,11 +13,15 @@ Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import this package.  It shares no code with the HIP path:
 the only common code is the seeded input generator, which holds none of the
 method's arithmetic.
+
+``qk_norm_ref`` is the query/key prologue that precedes the rotation in the
+served models (per-head RMS normalisation with a learned gain).
 """
 
 from .bf16 import bf16_bits_to_f64, f64_to_bf16_bits
 from .rope3d import RopeSpec, rope3d_ref, rope_angles
 from .attention import attn_ref, attn_ref_rows
+from .qknorm import qk_norm_ref
 
 __all__ = [
     "bf16_bits_to_f64",
@@ -27,4 +31,5 @@ __all__ = [
     "rope_angles",
     "attn_ref",
     "attn_ref_rows",
+    "qk_norm_ref",
 ]

@@ -76,3 +76,16 @@ def attention(q, k, v, scale, kv_valid_len=None, rope=None):
                     o[b][i][h][c] = math.fsum(w[j] * v[b][j][h][c] for j in range(lv)) / z
                 lse[b][h][i] = math.log(z)
     return o, lse
+
+
+def qk_norm_row(x, gain, eps, n, rope):
+    """RMS-normalise one head vector x (list of floats) by a math.fsum of its
+    squares, scale channel c by gain[c] (None: 1), then rotate it as token n
+    (rope = (grid, dims, theta, mode) or None)."""
+    d = len(x)
+    r = math.sqrt(math.fsum(v * v for v in x) / d + eps)
+    y = [x[c] / r * (1.0 if gain is None else gain[c]) for c in range(d)]
+    if rope is None:
+        return y
+    grid, dims, theta, mode = rope
+    return rope_row(y, n, grid, dims, theta, mode)

@@ -16,7 +16,12 @@ Sources of truth used here:
   * torch.nn.functional.scaled_dot_product_attention in float64 on the CPU as a
     library cross-check of the unmasked / prefix-masked attention;
   * invariants of softmax attention (single key, constant V, permutations,
-    shifts of all keys, Q = 0, one-hot limit, linearity in V, lse consistency).
+    shifts of all keys, Q = 0, one-hot limit, linearity in V, lse consistency);
+  * for the query/key prologue (RMS normalisation + gain + rotation): closed
+    forms of a constant vector (with eps dominant and negligible), unit RMS
+    of every (token, head) whatever the heads' own scales, invariance to a
+    positive scale, the gain as a per-channel factor, commutation of the
+    normalisation with the rotation, and the pure-Python brute force.
 """
 
 from __future__ import annotations
@@ -255,3 +260,85 @@ def check_attn_invariants(attn_fn, spec_cls):
 
 ALL_ROPE_CHECKS = [check_rope_unit_vectors, check_rope_known_frequency, check_rope_identities,
                    check_rope_relative, check_rope_brute]
+
+
+# ------------------------------------------------------ query/key prologue ---
+
+def check_norm_constant(norm_fn, spec_cls):
+    """x = c * 1 (all channels equal) becomes c / sqrt(c^2 + eps) in every
+    channel: eps negligible for c = +-3, dominant for c = 1e-5."""
+    for c, eps in [(3.0, 1e-6), (-3.0, 1e-6), (1e-5, 1e-6), (2.0, 0.0)]:
+        x = np.full((1, 2, 3, 8), c)
+        y = norm_fn(x, eps=eps)
+        assert np.allclose(y, c / math.sqrt(c * c + eps), rtol=1e-14, atol=0), (c, eps)
+
+
+def check_norm_unit_rms(norm_fn, spec_cls):
+    """With eps = 0 and unit gain every (token, head) vector leaves with mean
+    square 1, even when the heads (and tokens) carry very different scales."""
+    rng = _rng(41)
+    x = rng.standard_normal((2, 5, 4, 16)) * np.array([1e-3, 1.0, 7.0, 1e3])[None, None, :, None]
+    x = x * np.linspace(0.5, 4.0, 5)[None, :, None, None]
+    y = norm_fn(x, eps=0.0)
+    assert np.allclose(np.mean(y * y, axis=-1), 1.0, rtol=1e-13)
+    # direction kept: y is a positive multiple of x in each (token, head)
+    cos = np.sum(x * y, axis=-1) / (np.linalg.norm(x, axis=-1) * np.linalg.norm(y, axis=-1))
+    assert np.allclose(cos, 1.0, rtol=1e-13)
+
+
+def check_norm_scale_invariance(norm_fn, spec_cls):
+    """eps = 0: f(a x) = f(x) for a > 0 and f(-x) = -f(x)."""
+    rng = _rng(42)
+    x = rng.standard_normal((1, 6, 2, 12))
+    y = norm_fn(x, eps=0.0)
+    assert np.allclose(norm_fn(37.5 * x, eps=0.0), y, rtol=1e-13, atol=1e-14)
+    assert np.allclose(norm_fn(-x, eps=0.0), -y, rtol=1e-13, atol=1e-14)
+
+
+def check_norm_gain(norm_fn, spec_cls):
+    """The gain multiplies channel c of every head by g[c]; a one-hot gain
+    keeps one channel only."""
+    rng = _rng(43)
+    x = rng.standard_normal((2, 3, 2, 12))
+    g = rng.uniform(0.5, 2.0, 12)
+    base = norm_fn(x, eps=1e-6)
+    assert np.allclose(norm_fn(x, gain=g, eps=1e-6), base * g, rtol=1e-14, atol=1e-15)
+    oh = np.zeros(12)
+    oh[5] = 2.0
+    y = norm_fn(x, gain=oh, eps=1e-6)
+    assert np.all(y[..., np.arange(12) != 5] == 0.0)
+    assert np.allclose(y[..., 5], 2.0 * base[..., 5], rtol=1e-14)
+
+
+def check_norm_rope_commute(norm_fn, spec_cls):
+    """With unit gain the normalisation commutes with the rotation, which keeps
+    every pair's norm: normalising x rotated by the brute-force rotation equals
+    normalise-then-rotate."""
+    rng = _rng(44)
+    grid, dims, theta = (2, 2, 3), (4, 4, 4), 100.0
+    spec = spec_cls(grid=grid, dims=dims, theta=theta, pair_mode=0)
+    x = rng.standard_normal((1, 14, 2, 12))  # 12 rotated tokens, 2 beyond the grid
+    xr = np.array([[[brute.rope_row(list(x[0, n, h]), n, grid, dims, theta, 0) for h in range(2)] for n in range(14)]])
+    assert not np.allclose(xr, x)
+    assert np.allclose(norm_fn(xr, eps=1e-6), norm_fn(x, eps=1e-6, rope=spec), rtol=1e-12, atol=1e-13)
+
+
+def check_norm_brute(norm_fn, spec_cls):
+    """Element-wise agreement with the pure-Python brute force (fsum of
+    squares, complex rotation), with and without gain and rotation."""
+    rng = _rng(45)
+    B, L, H, d = 2, 9, 2, 12
+    x = rng.standard_normal((B, L, H, d)) * 3.0
+    g = rng.uniform(0.5, 1.5, d)
+    for gain, rope in [(None, None), (g, None), (g, ((2, 2, 2), (4, 4, 4), 30.0, 0)), (None, ((1, 3, 2), (2, 4, 6), 7.0, 1))]:
+        spec = None if rope is None else spec_cls(grid=rope[0], dims=rope[1], theta=rope[2], pair_mode=rope[3])
+        y = norm_fn(x, gain=gain, eps=1e-3, rope=spec)
+        for b in range(B):
+            for n in range(L):
+                for h in range(H):
+                    want = brute.qk_norm_row(list(x[b, n, h]), None if gain is None else list(gain), 1e-3, n, rope)
+                    assert np.allclose(y[b, n, h], want, rtol=1e-12, atol=1e-13), (b, n, h)
+
+
+ALL_NORM_CHECKS = [check_norm_constant, check_norm_unit_rms, check_norm_scale_invariance, check_norm_gain,
+                   check_norm_rope_commute, check_norm_brute]

@@ -141,3 +141,79 @@ def test_attn_mutation_is_caught(name, monkeypatch):
     attr, fn = ATTN_MUTATIONS[name]
     monkeypatch.setattr(oa, attr, fn)
     assert _any_attn_pin_fails(), name
+
+
+# ------------------------------------------------------ query/key prologue ---
+
+import oracle.qknorm as oq  # noqa: E402
+
+_ORIG_MS = oq.mean_square
+_ORIG_RS = oq.rms_scale
+
+
+def _ms_sum_not_mean(x):
+    return np.sum(x * x, axis=-1, keepdims=True)
+
+
+def _ms_over_heads_and_channels(x):
+    return np.mean(x * x, axis=(-2, -1), keepdims=True)
+
+
+def _ms_over_tokens(x):
+    return np.mean(x * x, axis=(1, -1), keepdims=True)
+
+
+def _ms_abs_not_square(x):
+    return np.mean(np.abs(x), axis=-1, keepdims=True) ** 2
+
+
+def _rs_eps_outside(ms, eps):
+    return 1.0 / (np.sqrt(ms) + eps)
+
+
+def _rs_no_sqrt(ms, eps):
+    return 1.0 / (ms + eps)
+
+
+def _rs_eps_ignored(ms, eps):
+    return 1.0 / np.sqrt(ms)
+
+
+NORM_MUTATIONS = {
+    "sum_of_squares_not_mean": ("mean_square", _ms_sum_not_mean),
+    "norm_over_all_heads": ("mean_square", _ms_over_heads_and_channels),
+    "norm_over_tokens": ("mean_square", _ms_over_tokens),
+    "mean_abs_squared": ("mean_square", _ms_abs_not_square),
+    "eps_outside_sqrt": ("rms_scale", _rs_eps_outside),
+    "missing_sqrt": ("rms_scale", _rs_no_sqrt),
+    "eps_ignored": ("rms_scale", _rs_eps_ignored),
+}
+
+
+def _any_norm_pin_fails():
+    for check in pins.ALL_NORM_CHECKS:
+        try:
+            check(oq.qk_norm_ref, RopeSpec)
+        except AssertionError:
+            return True
+    return False
+
+
+@pytest.mark.parametrize("name", sorted(NORM_MUTATIONS))
+def test_norm_mutation_is_caught(name, monkeypatch):
+    attr, fn = NORM_MUTATIONS[name]
+    monkeypatch.setattr(oq, attr, fn)
+    assert _any_norm_pin_fails(), name
+
+
+def test_norm_gain_dropped_is_caught(monkeypatch):
+    orig = oq.qk_norm_ref
+
+    def no_gain(x, gain=None, eps=1e-6, rope=None, token_index=None):
+        return orig(x, None, eps, rope, token_index)
+
+    try:
+        pins.check_norm_gain(no_gain, RopeSpec)
+    except AssertionError:
+        return
+    raise AssertionError("dropping the gain went unnoticed")

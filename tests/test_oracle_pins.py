@@ -50,3 +50,8 @@ def test_bf16_codec():
     x = np.array([1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, 1.0 + 2 ** -8 + 2 ** -30, -2.5])
     r = oracle.bf16_bits_to_f64(oracle.f64_to_bf16_bits(x))
     assert list(r) == [1.0, 1.0 + 2 ** -6, 1.0 + 2 ** -7, -2.5]
+
+
+@pytest.mark.parametrize("check", pins.ALL_NORM_CHECKS, ids=lambda c: c.__name__)
+def test_norm_pins(check):
+    check(oracle.qk_norm_ref, oracle.RopeSpec)
