@@ -140,6 +140,39 @@ def time_gpu(w, steps, warmup, fused=False):
     }
 
 
+def time_prologues(w, steps):
+    """The HBM-bound kernels on one [B, L, H, d] tensor of the workload:
+    vidax_rope3d and vidax_qk_norm_rope (RMS norm + gain + rotation), each one
+    read and one write of the tensor."""
+    import torch
+
+    import paper_2609_18077_amd as vx
+    from paper_2609_18077_amd import inputs
+
+    x = torch.from_numpy(inputs.bf16_tensor(w.seed, inputs.T_K, (w.B, w.Lk, w.H, w.d)).view(np.int16)).cuda()
+    x = x.view(torch.bfloat16)
+    y = torch.empty_like(x)
+    g = torch.ones(w.d, dtype=torch.float32, device="cuda")
+    rope = vx.Rope(w.grid, w.dims, w.theta)
+    out = {}
+    for name, fn in [("rope3d_" + w.name, lambda: vx.rope3d(x, rope, out=y)),
+                     ("qk_norm_rope_" + w.name, lambda: vx.qk_norm_rope(x, rope, gain=g, out=y))]:
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        gbs = 2 * x.numel() * 2 / (ms * 1e-3) / 1e9
+        out[name] = {"ms": ms, "algorithmic_GBs": gbs, "pct_hbm_peak": 100 * gbs / PEAK_HBM_GBS}
+        log(f"[bench] {name:28s} {ms * 1e3:8.1f} us  {gbs:8.1f} GB/s  {100 * gbs / PEAK_HBM_GBS:5.1f}% of HBM")
+    return out
+
+
 def cpu_baseline(w, q, k, v, lv, budget_s=12.0):
     """The fp64 oracle on a bounded sample: whole heads of the same workload,
     all query rows, one head at a time until the time budget is used."""
@@ -246,6 +279,7 @@ def main():
             log(f"[bench] {name:14s} {rows[name]['ms']:9.3f} ms  {rows[name]['tflops']:8.1f} TFLOP/s  "
                 f"{rows[name]['pct_bf16_peak']:5.1f}%  {rows[name]['algorithmic_GBs']:8.1f} GB/s")
             torch.cuda.empty_cache()
+        rows.update(time_prologues(inputs.WORKLOADS["wan13b_480p"], max(5, args.steps // 2)))
         os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
         with open(os.path.join(ROOT, "gpurun_out", "bench_all.json"), "w") as f:
             json.dump(rows, f, indent=1)

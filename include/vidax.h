@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define VIDAX_ABI_VERSION 2
+#define VIDAX_ABI_VERSION 3
 
 typedef enum vidax_status {
   VIDAX_OK = 0,
@@ -88,6 +88,28 @@ typedef struct vidax_rope3d_desc {
  */
 vidax_status vidax_rope3d(const void* x, void* y, int32_t B, int32_t L, int32_t H, int32_t d,
                           const vidax_rope3d_desc* rope, hipStream_t stream);
+
+/*
+ * Query/key prologue of the served 3D-RoPE models (Section 3, "Supported
+ * Models"; the paper gives no formula, the standard RMS normalisation is
+ * used):  for every (batch, token, head) row x of d channels
+ *
+ *   y[c] = rope3d( x[c] / sqrt(mean_c'(x[c']^2) + eps) * gain[c] )
+ *
+ * computed in fp32 from the bf16 input and rounded to bf16 once.
+ *   x, y : bf16 [B, L, H, d] (device); x == y (in place) is allowed, other
+ *          overlap is not.
+ *   gain : fp32 [d] on the device, shared by all heads, 16-byte aligned; or
+ *          NULL for unit gain.
+ *   eps  : >= 0 and finite (e.g. 1e-6); an all-zero row with eps = 0 gives NaN.
+ *   rope : host pointer to a descriptor (as vidax_rope3d; pair_mode 0 only,
+ *          VIDAX_ERR_UNSUPPORTED otherwise; keys_prerotated is ignored), or
+ *          NULL for normalisation and gain only.
+ * Requires d == 128 (VIDAX_ERR_UNSUPPORTED otherwise); B, L, H >= 0
+ * (zero-sized calls are no-ops).  HBM-bound: one read and one write of x.
+ */
+vidax_status vidax_qk_norm_rope(const void* x, void* y, const float* gain, float eps, int32_t B, int32_t L,
+                                int32_t H, int32_t d, const vidax_rope3d_desc* rope, hipStream_t stream);
 
 /*
  * o = softmax(scale * rope(q) rope(k)^T + mask) v, per batch b and head h.

@@ -21,6 +21,7 @@ _STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported configuration", 3: "k
 
 EXPORTED_SYMBOLS = (
     "vidax_rope3d",
+    "vidax_qk_norm_rope",
     "vidax_attn_fwd",
     "vidax_attn_fwd_naive",
     "vidax_status_string",
@@ -80,6 +81,8 @@ def lib() -> ctypes.CDLL:
         vp, i32, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float
         L.vidax_rope3d.argtypes = [vp, vp, i32, i32, i32, i32, ctypes.POINTER(RopeDesc), vp]
         L.vidax_rope3d.restype = i32
+        L.vidax_qk_norm_rope.argtypes = [vp, vp, vp, f32, i32, i32, i32, i32, ctypes.POINTER(RopeDesc), vp]
+        L.vidax_qk_norm_rope.restype = i32
         for name in ("vidax_attn_fwd", "vidax_attn_fwd_naive"):
             fn = getattr(L, name)
             fn.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, f32, vp, ctypes.POINTER(RopeDesc), vp]
@@ -127,6 +130,28 @@ def rope3d(x, rope: Rope, out=None, stream=None):
     B, L, H, d = x.shape
     desc = rope.desc()
     _check("vidax_rope3d", lib().vidax_rope3d(_ptr(x), _ptr(y), B, L, H, d, ctypes.byref(desc), _stream(stream)))
+    return y
+
+
+def qk_norm_rope(x, rope: Rope | None = None, gain=None, eps: float = 1e-6, out=None, stream=None):
+    """Per-(token, head) RMS normalisation of x (bf16 [B, L, H, d]), channel
+    gain (fp32 [d] device tensor or None), then the 3D rotation (or none);
+    out may be x itself (in place)."""
+    import torch
+
+    _check_bshd("x", x)
+    y = torch.empty_like(x) if out is None else out
+    _check_bshd("out", y)
+    if y.shape != x.shape:
+        raise ValueError("out must have the shape of x")
+    B, L, H, d = x.shape
+    if gain is not None:
+        if gain.dtype != torch.float32 or not gain.is_cuda or not gain.is_contiguous() or gain.numel() != d:
+            raise ValueError("gain must be a contiguous float32 device tensor of d elements")
+    desc = rope.desc() if rope is not None else None
+    _check("vidax_qk_norm_rope", lib().vidax_qk_norm_rope(_ptr(x), _ptr(y), _ptr(gain), float(eps), B, L, H, d,
+                                                          ctypes.byref(desc) if desc is not None else None,
+                                                          _stream(stream)))
     return y
 
 

@@ -92,6 +92,8 @@ __host__ __device__ inline PairSlot pair_slot(const RopeParams& r, int pi) {
 namespace vidax {
 hipError_t launch_rope3d(const uint16_t* x, uint16_t* y, int B, int L, int H, const RopeParams& rp,
                          hipStream_t stream);
+hipError_t launch_qk_norm(const uint16_t* x, uint16_t* y, const float* gain, float eps, int B, int L, int H,
+                          const RopeParams& rp, hipStream_t stream);
 hipError_t launch_attn_naive(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o,
                              float* lse, int B, int H, int Lq, int Lk, float scale,
                              const int32_t* kv_valid_len, const RopeParams& rp, hipStream_t stream);

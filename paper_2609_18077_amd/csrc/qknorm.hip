@@ -1,0 +1,128 @@
+// Query/key prologue, bf16 [B, L, H, 128] -> bf16 (HBM-bound): per-(token,
+// head) RMS normalisation in fp32, a per-channel gain shared by all heads, the
+// 3D rotation (interleaved pairs), rounding to bf16.
+//
+// Layout as in the standalone rotary kernel: the 16 channel chunks (16 B)
+// of a (token, head) row go to 16 consecutive lanes; a lane decodes its
+// token's (t, h, w) once, fetches the four (cos, sin) pairs of its chunk and
+// handles that chunk for every batch and head of the token.  A row's sum of
+// squares is combined across its 16 lanes with data-parallel lane moves
+// (rotations within the 16-lane row, then permutations within quads), so
+// each lane ends with the row total without touching LDS.  Every lane reads
+// its chunk before any lane of the row writes, so y may alias x.
+#include "common.hpp"
+
+namespace vidax {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kTokensPerPass = kThreads / 16;
+
+struct QkNormArgs {
+  const uint16_t* x;
+  uint16_t* y;
+  const float* gain;  // [128] or null (unit gain)
+  float eps;
+  int B, L, H;
+  RopeParams rp;
+};
+
+// v summed over the 16 lanes of its row; every lane receives the sum.
+__device__ __forceinline__ float row16_sum(float v) {
+  // row_ror:8, row_ror:4, quad_perm [2,3,0,1], quad_perm [1,0,3,2]
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x128, 0xf, 0xf, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x124, 0xf, 0xf, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4e, 0xf, 0xf, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xb1, 0xf, 0xf, false));
+  return v;
+}
+
+template <bool ROPE>
+__global__ __launch_bounds__(kThreads) void qk_norm_kernel(QkNormArgs a) {
+  __shared__ float2 tab[ROPE ? kRopeTableMax : 1];
+  const RopeParams& rp = a.rp;
+  if (ROPE) {
+    for (int e = threadIdx.x; e < rp.n_entries; e += kThreads) tab[e] = rope_table_entry(rp, e);
+    __syncthreads();
+  }
+
+  const int c = threadIdx.x & 15;  // chunk: channels 8c .. 8c + 7 = pairs 4c .. 4c + 3
+  float g[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) g[e] = 1.f;
+  if (a.gain) {
+    const float4 g0 = *reinterpret_cast<const float4*>(a.gain + 8 * c);
+    const float4 g1 = *reinterpret_cast<const float4*>(a.gain + 8 * c + 4);
+    g[0] = g0.x; g[1] = g0.y; g[2] = g0.z; g[3] = g0.w;
+    g[4] = g1.x; g[5] = g1.y; g[6] = g1.z; g[7] = g1.w;
+  }
+  PairSlot slot[4];
+  if (ROPE) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) slot[p] = pair_slot(rp, 4 * c + p);
+  }
+  const size_t tok_stride = (size_t)a.H * kHeadDim;      // elements between tokens
+  const size_t batch_stride = (size_t)a.L * tok_stride;  // elements between batches
+  const float inv_d = 1.0f / kHeadDim;
+
+  for (int n = blockIdx.x * kTokensPerPass + (threadIdx.x >> 4); n < a.L; n += gridDim.x * kTokensPerPass) {
+    const bool rot = ROPE && n < rp.n_rot;
+    float cs[4] = {1.f, 1.f, 1.f, 1.f}, sn[4] = {0.f, 0.f, 0.f, 0.f};
+    if (rot) {
+      const int t = n / (rp.gh * rp.gw);
+      const int r = n - t * rp.gh * rp.gw;
+      const int h = r / rp.gw;
+      const int w = r - h * rp.gw;
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const int pos = slot[p].axis == 0 ? t : (slot[p].axis == 1 ? h : w);
+        const float2 e = tab[slot[p].base + pos * slot[p].stride];
+        cs[p] = e.x;
+        sn[p] = e.y;
+      }
+    }
+    for (int b = 0; b < a.B; ++b) {
+      const size_t row0 = b * batch_stride + (size_t)n * tok_stride + c * 8;
+      for (int hh = 0; hh < a.H; ++hh) {
+        const size_t off = row0 + (size_t)hh * kHeadDim;
+        const uint4 v = *reinterpret_cast<const uint4*>(a.x + off);
+        const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+        float xf[8];
+        float ss = 0.f;
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          xf[2 * p] = bf16lo_to_f32(wv[p]);
+          xf[2 * p + 1] = bf16hi_to_f32(wv[p]);
+          ss = fmaf(xf[2 * p], xf[2 * p], ss);
+          ss = fmaf(xf[2 * p + 1], xf[2 * p + 1], ss);
+        }
+        const float r = rsqrtf(fmaf(row16_sum(ss), inv_d, a.eps));
+        uint32_t o[4];
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          const float y0 = xf[2 * p] * r * g[2 * p];
+          const float y1 = xf[2 * p + 1] * r * g[2 * p + 1];
+          o[p] = rot ? pack_bf16x2(fmaf(y0, cs[p], -y1 * sn[p]), fmaf(y0, sn[p], y1 * cs[p])) : pack_bf16x2(y0, y1);
+        }
+        *reinterpret_cast<uint4*>(a.y + off) = make_uint4(o[0], o[1], o[2], o[3]);
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_qk_norm(const uint16_t* x, uint16_t* y, const float* gain, float eps, int B, int L, int H,
+                          const RopeParams& rp, hipStream_t stream) {
+  QkNormArgs a{x, y, gain, eps, B, L, H, rp};
+  int groups = (L + kTokensPerPass - 1) / kTokensPerPass;
+  int grid = groups < 2048 ? groups : 2048;
+  if (grid < 1) grid = 1;
+  if (rp.enabled)
+    hipLaunchKernelGGL(qk_norm_kernel<true>, dim3(grid), dim3(kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(qk_norm_kernel<false>, dim3(grid), dim3(kThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace vidax

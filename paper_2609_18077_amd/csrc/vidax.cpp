@@ -118,6 +118,30 @@ vidax_status attn_common(AttnImpl impl, const void* q, const void* k, const void
 
 extern "C" {
 
+vidax_status vidax_qk_norm_rope(const void* x, void* y, const float* gain, float eps, int32_t B, int32_t L, int32_t H,
+                                int32_t d, const vidax_rope3d_desc* rope, hipStream_t stream) {
+  if (B < 0 || L < 0 || H < 0 || d < 0) return VIDAX_ERR_INVALID_ARG;
+  const int64_t n = numel4(B, L, H, d);
+  if (n < 0) return VIDAX_ERR_INVALID_ARG;
+  if (n > 0 && (!x || !y)) return VIDAX_ERR_INVALID_ARG;
+  if (!aligned(x, 16) || !aligned(y, 16) || !aligned(gain, 16)) return VIDAX_ERR_INVALID_ARG;
+  if (!(eps >= 0.0f) || !isfinite(eps)) return VIDAX_ERR_INVALID_ARG;
+  if (d != vidax::kHeadDim) return VIDAX_ERR_UNSUPPORTED;
+  if (x != y && overlaps(x, (uint64_t)n * 2, y, (uint64_t)n * 2)) return VIDAX_ERR_INVALID_ARG;
+  if (gain && overlaps(gain, (uint64_t)d * 4, y, (uint64_t)n * 2)) return VIDAX_ERR_INVALID_ARG;
+  RopeParams rp = no_rope();
+  if (rope) {
+    vidax_rope3d_desc r = *rope;
+    r.keys_prerotated = 0;  // attention-only field
+    const vidax_status st = make_rope(&r, L, d, &rp);
+    if (st != VIDAX_OK) return st;
+    if (rp.pair_mode != 0) return VIDAX_ERR_UNSUPPORTED;
+  }
+  if (B == 0 || L == 0 || H == 0) return VIDAX_OK;
+  const hipError_t e = vidax::launch_qk_norm((const uint16_t*)x, (uint16_t*)y, gain, eps, B, L, H, rp, stream);
+  return e == hipSuccess ? VIDAX_OK : VIDAX_ERR_LAUNCH;
+}
+
 vidax_status vidax_rope3d(const void* x, void* y, int32_t B, int32_t L, int32_t H, int32_t d,
                           const vidax_rope3d_desc* rope, hipStream_t stream) {
   if (B < 0 || L < 0 || H < 0 || d < 0) return VIDAX_ERR_INVALID_ARG;

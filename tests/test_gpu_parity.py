@@ -128,6 +128,79 @@ def test_rope3d_full_size_wan13b():
     assert np.all(np.abs(got - ref) <= _rope_bound(oracle.bf16_bits_to_f64(k[:, rows]), ref, spec_of(w), rows))
 
 
+# ------------------------------------------------- query/key prologue ---
+
+def _norm_bound(x, gain, eps, ref, spec, rows):
+    """One bf16 ulp of the result, the fp32 normalisation (sum of 128 squares,
+    reciprocal square root, two products: relative 2^-16 at most) and, for
+    rotated tokens, the rotation's fp32 error as in _rope_bound, all relative
+    to the normalised pair's norm."""
+    y = oracle.qk_norm_ref(x, gain=gain, eps=eps)
+    if spec is None:
+        return _ulp_bf16(ref) + 2.0 ** -16 * np.abs(y) + 1e-30
+    norm, ang = _pair_norm_and_angle(y, spec, rows)
+    return _ulp_bf16(ref) + (2.0 ** -16 + 2.0 ** -20 * (1.0 + ang)) * norm + 1e-30
+
+
+def _head_scaled(seed, shape, exps):
+    """bf16 N(0,1) tensor with head h scaled by 2**exps[h] (exact in bf16)."""
+    x = oracle.bf16_bits_to_f64(inputs.bf16_tensor(seed, 0, shape))
+    x = x * (2.0 ** np.asarray(exps, np.float64))[None, None, :, None]
+    return oracle.f64_to_bf16_bits(x)
+
+
+@pytest.mark.parametrize("rotate,with_gain,inplace", [(False, False, False), (False, True, False),
+                                                     (True, True, False), (True, False, True)])
+def test_qk_norm_rope_matches_oracle(rotate, with_gain, inplace):
+    import torch
+
+    grid = (3, 10, 30)  # 900 video tokens, then 100 unrotated tokens
+    x = _head_scaled(12, (2, 1000, 3, 128), [-6, 0, 5])
+    g = np.random.default_rng(13).uniform(0.5, 1.5, 128).astype(np.float32)
+    eps = 1e-6
+    log(f"case qk_norm_rope rotate={rotate} gain={with_gain} inplace={inplace}")
+    xd = to_dev(x)
+    gd = torch.from_numpy(g).cuda() if with_gain else None
+    r = vx.Rope(grid=grid, dims=(44, 42, 42), theta=10000.0) if rotate else None
+    y = vx.qk_norm_rope(xd, r, gain=gd, eps=eps, out=xd if inplace else None)
+    torch.cuda.synchronize()
+    got = oracle.bf16_bits_to_f64(to_bits(y))
+    spec = oracle.RopeSpec(grid=grid) if rotate else None
+    xf = oracle.bf16_bits_to_f64(x)
+    gain = g.astype(np.float64) if with_gain else None
+    ref = oracle.qk_norm_ref(xf, gain=gain, eps=eps, rope=spec)
+    err = np.abs(got - ref)
+    bound = _norm_bound(xf, gain, eps, ref, spec, np.arange(x.shape[1]))
+    assert np.all(err <= bound), (err.max(), float((err / bound).max()))
+    exact = np.mean(to_bits(y) == oracle.f64_to_bf16_bits(ref))
+    log(f"  correctly rounded fraction {exact:.5f}")
+    assert exact > 0.99
+
+
+def test_qk_norm_rope_full_size_wan13b():
+    import torch
+
+    w = inputs.WORKLOADS["wan13b_480p"]
+    k = inputs.bf16_tensor(w.seed, inputs.T_K, (w.B, w.Lk, w.H, w.d))  # before normalisation
+    g = np.random.default_rng(14).uniform(0.5, 1.5, 128).astype(np.float32)
+    log("case qk_norm_rope wan13b_480p K")
+    y = vx.qk_norm_rope(to_dev(k), rope_of(w), gain=torch.from_numpy(g).cuda(), eps=1e-6)
+    torch.cuda.synchronize()
+    yb = to_bits(y)
+    rows = np.unique(np.r_[0, 1, 51, 52, 1559, 1560, w.Lk - 1, np.random.default_rng(0).integers(0, w.Lk, 300)])
+    xf = oracle.bf16_bits_to_f64(k[:, rows])
+    ref = oracle.qk_norm_ref(xf, gain=g.astype(np.float64), eps=1e-6, rope=spec_of(w), token_index=rows)
+    got = oracle.bf16_bits_to_f64(yb[:, rows])
+    assert np.all(np.abs(got - ref) <= _norm_bound(xf, g.astype(np.float64), 1e-6, ref, spec_of(w), rows))
+
+
+def test_qk_norm_rope_empty():
+    import torch
+
+    x = torch.empty((0, 5, 2, 128), dtype=torch.bfloat16, device="cuda")
+    assert vx.qk_norm_rope(x).shape == x.shape
+
+
 # ------------------------------------------------------- attention: small ---
 
 def test_tiny_workload():

@@ -25,7 +25,7 @@ def test_library_exports_every_declared_function():
     assert set(declared) == set(vx.EXPORTED_SYMBOLS), declared
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.vidax_abi_version() == 2
+    assert lib.vidax_abi_version() == 3
     for s, text in [(0, b"ok"), (1, b"invalid argument"), (2, b"unsupported configuration"), (3, b"kernel launch failed")]:
         assert lib.vidax_status_string(s) == text
     assert lib.vidax_status_string(99) == b"unknown status"
@@ -98,6 +98,30 @@ def test_rope3d_rejects_invalid_arguments():
     assert call(L=63) == 1                    # 64 rotated tokens > L
     assert call(y=P + 256) == 1               # partial overlap (in place is x == y)
     assert call(rope=vx.Rope((2, 4, 8), (42, 42, 42)).desc()) == 1
+
+
+def test_qk_norm_rope_rejects_invalid_arguments():
+    f = vx.lib().vidax_qk_norm_rope
+    good = vx.Rope((2, 4, 8), (44, 42, 42)).desc()
+
+    def call(x=P, y=2 * P, gain=3 * P, eps=1e-6, B=1, L=64, H=2, d=128, rope=good):
+        return f(ctypes.c_void_p(x), ctypes.c_void_p(y), ctypes.c_void_p(gain) if gain else None, eps, B, L, H, d,
+                 ctypes.byref(rope) if rope is not None else None, None)
+
+    assert call(x=0) == 1
+    assert call(x=0, y=0, L=0, rope=None) == 0       # empty: no-op, NULL allowed
+    assert call(y=2 * P + 2) == 1                    # misaligned output
+    assert call(gain=3 * P + 4) == 1                 # misaligned gain
+    assert call(eps=-1e-6) == 1
+    assert call(eps=float("nan")) == 1
+    assert call(eps=float("inf")) == 1
+    assert call(L=-1) == 1
+    assert call(d=64) == 2
+    assert call(L=63) == 1                           # 64 rotated tokens > L
+    assert call(y=P + 256) == 1                      # partial overlap (in place is x == y)
+    assert call(gain=2 * P + 512) == 1               # gain overlaps the output
+    assert call(rope=vx.Rope((2, 4, 8), (44, 42, 42), pair_mode=1).desc()) == 2  # half split: unsupported
+    assert call(rope=vx.Rope((2, 4, 8), (40, 42, 42)).desc()) == 1               # widths do not sum to d
 
 
 def test_binding_fails_loudly_without_library(monkeypatch):
