@@ -15,13 +15,16 @@ the only common code is the seeded input generator, which holds none of the
 method's arithmetic.
 
 ``qk_norm_ref`` is the query/key prologue that precedes the rotation in the
-served models (per-head RMS normalisation with a learned gain).
+served models (per-head RMS normalisation with a learned gain);
+``attn_bwd_ref`` is the gradient of the attention (for post-training), and
+``rope_transpose_ref`` carries a gradient back through the rotation.
 """
 
 from .bf16 import bf16_bits_to_f64, f64_to_bf16_bits
 from .rope3d import RopeSpec, rope3d_ref, rope_angles
 from .attention import attn_ref, attn_ref_rows
 from .qknorm import qk_norm_ref
+from .attention_bwd import attn_bwd_ref, rope_transpose_ref
 
 __all__ = [
     "bf16_bits_to_f64",
@@ -32,4 +35,6 @@ __all__ = [
     "attn_ref",
     "attn_ref_rows",
     "qk_norm_ref",
+    "attn_bwd_ref",
+    "rope_transpose_ref",
 ]

@@ -21,7 +21,12 @@ Sources of truth used here:
     forms of a constant vector (with eps dominant and negligible), unit RMS
     of every (token, head) whatever the heads' own scales, invariance to a
     positive scale, the gain as a per-channel factor, commutation of the
-    normalisation with the rotation, and the pure-Python brute force.
+    normalisation with the rotation, and the pure-Python brute force;
+  * for the attention gradient: central finite differences of the (pinned)
+    forward oracle, torch autograd in float64, and identities of the softmax
+    gradient (sum of dK over keys is zero, sum of dV over keys is the sum of
+    dO, linearity in dO, zero gradient of masked keys and of empty batches),
+    plus the adjoint identity of the rotation's transpose.
 """
 
 from __future__ import annotations
@@ -342,3 +347,92 @@ def check_norm_brute(norm_fn, spec_cls):
 
 ALL_NORM_CHECKS = [check_norm_constant, check_norm_unit_rms, check_norm_scale_invariance, check_norm_gain,
                    check_norm_rope_commute, check_norm_brute]
+
+
+# ------------------------------------------------------ attention gradient ---
+
+def _bwd_case(rng, B=2, Lq=5, Lk=6, H=2, d=8):
+    q = rng.standard_normal((B, Lq, H, d))
+    k = rng.standard_normal((B, Lk, H, d))
+    v = rng.standard_normal((B, Lk, H, d))
+    do = rng.standard_normal((B, Lq, H, d))
+    return q, k, v, do
+
+
+def check_bwd_finite_diff(bwd_fn, fwd_fn):
+    """Central differences of L = sum(dO * attn(q, k, v)) match every element
+    of dq, dk, dv, with a masked key prefix in one batch."""
+    rng = _rng(51)
+    q, k, v, do = _bwd_case(rng)
+    sc, lv = 0.6, np.array([6, 4])
+    dq, dk, dv = bwd_fn(q, k, v, do, sc, kv_valid_len=lv)
+
+    def loss(q_, k_, v_):
+        return float(np.sum(do * fwd_fn(q_, k_, v_, sc, kv_valid_len=lv)[0]))
+
+    h = 1e-6
+    for name, x, g in (("q", q, dq), ("k", k, dk), ("v", v, dv)):
+        num = np.zeros_like(x)
+        for idx in np.ndindex(x.shape):
+            xp, xm = x.copy(), x.copy()
+            xp[idx] += h
+            xm[idx] -= h
+            args_p = {"q": (xp, k, v), "k": (q, xp, v), "v": (q, k, xp)}[name]
+            args_m = {"q": (xm, k, v), "k": (q, xm, v), "v": (q, k, xm)}[name]
+            num[idx] = (loss(*args_p) - loss(*args_m)) / (2 * h)
+        assert np.allclose(g, num, rtol=1e-6, atol=1e-7), (name, np.abs(g - num).max())
+
+
+def check_bwd_torch(bwd_fn, fwd_fn):
+    """torch autograd through float64 SDPA (prefix mask as an additive mask)."""
+    import torch
+
+    rng = _rng(52)
+    q, k, v, do = _bwd_case(rng, B=2, Lq=7, Lk=9, H=3, d=16)
+    sc, lv = 0.3, np.array([9, 5])
+    dq, dk, dv = bwd_fn(q, k, v, do, sc, kv_valid_len=lv)
+    tq, tk, tv = (torch.tensor(x.transpose(0, 2, 1, 3), requires_grad=True) for x in (q, k, v))
+    mask = torch.zeros((2, 1, 7, 9), dtype=torch.float64)
+    mask[1, :, :, 5:] = -math.inf
+    out = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, attn_mask=mask, scale=sc)
+    out.backward(torch.tensor(do.transpose(0, 2, 1, 3)))
+    for g, t in ((dq, tq), (dk, tk), (dv, tv)):
+        assert np.allclose(g, t.grad.numpy().transpose(0, 2, 1, 3), rtol=1e-10, atol=1e-12)
+
+
+def check_bwd_identities(bwd_fn, fwd_fn):
+    rng = _rng(53)
+    q, k, v, do = _bwd_case(rng, B=3, Lq=6, Lk=8, H=2, d=8)
+    sc, lv = 0.8, np.array([8, 3, 0])
+    dq, dk, dv = bwd_fn(q, k, v, do, sc, kv_valid_len=lv)
+    # shifting every key by one vector leaves the output unchanged: sum_j dK_j = 0
+    assert np.allclose(dk.sum(axis=1), 0.0, atol=1e-12)
+    # softmax weights sum to one: sum_j dV_j = sum_i dO_i (batches with keys)
+    for b in range(2):
+        assert np.allclose(dv[b].sum(axis=0), do[b].sum(axis=0), rtol=1e-12, atol=1e-12)
+    # masked keys and empty batches get exactly zero gradient
+    assert np.all(dk[1, 3:] == 0) and np.all(dv[1, 3:] == 0)
+    assert np.all(dq[2] == 0) and np.all(dk[2] == 0) and np.all(dv[2] == 0)
+    # linear in dO
+    do2 = rng.standard_normal(do.shape)
+    g1 = bwd_fn(q, k, v, 2.0 * do - 0.5 * do2, sc, kv_valid_len=lv)
+    g2 = bwd_fn(q, k, v, do2, sc, kv_valid_len=lv)
+    for a, b_, c in zip(g1, (dq, dk, dv), g2):
+        assert np.allclose(a, 2.0 * b_ - 0.5 * c, rtol=1e-11, atol=1e-12)
+
+
+def check_rope_transpose(transpose_fn, rope_fn, spec_cls):
+    """<R x, y> = <x, R^T y> for every token and head; R^T R x = x."""
+    rng = _rng(54)
+    for mode in (0, 1):
+        spec = spec_cls(grid=(2, 3, 2), dims=(4, 4, 4), theta=30.0, pair_mode=mode)
+        x = rng.standard_normal((2, 14, 2, 12))
+        y = rng.standard_normal((2, 14, 2, 12))
+        lhs = np.sum(rope_fn(x, spec) * y, axis=-1)
+        rhs = np.sum(x * transpose_fn(y, spec), axis=-1)
+        assert np.allclose(lhs, rhs, rtol=1e-12, atol=1e-12)
+        assert np.allclose(transpose_fn(rope_fn(x, spec), spec), x, rtol=1e-12, atol=1e-12)
+        assert not np.allclose(transpose_fn(y, spec), rope_fn(y, spec))
+
+
+ALL_BWD_CHECKS = [check_bwd_finite_diff, check_bwd_torch, check_bwd_identities]

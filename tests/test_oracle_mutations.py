@@ -217,3 +217,75 @@ def test_norm_gain_dropped_is_caught(monkeypatch):
     except AssertionError:
         return
     raise AssertionError("dropping the gain went unnoticed")
+
+
+# ------------------------------------------------------ attention gradient ---
+
+import oracle.attention_bwd as ob  # noqa: E402
+from oracle import attn_bwd_ref  # noqa: E402
+
+_ORIG_HEAD = ob._one_head
+
+
+def _softmax(s):
+    e = np.exp(s - s.max(axis=1, keepdims=True))
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def _head_no_delta(q, k, v, do, scale):
+    p = _softmax(scale * (q @ k.T))
+    ds = p * (do @ v.T)
+    return scale * (ds @ k), scale * (ds.T @ q), p.T @ do
+
+
+def _head_delta_wrong_axis(q, k, v, do, scale):
+    p = _softmax(scale * (q @ k.T))
+    dp = do @ v.T
+    ds = p * (dp - np.sum(p * dp, axis=0, keepdims=True))
+    return scale * (ds @ k), scale * (ds.T @ q), p.T @ do
+
+
+def _head_dq_unscaled(q, k, v, do, scale):
+    dq, dk, dv = _ORIG_HEAD(q, k, v, do, scale)
+    return dq / scale, dk, dv
+
+
+def _head_dk_uses_keys(q, k, v, do, scale):
+    p = _softmax(scale * (q @ k.T))
+    dp = do @ v.T
+    ds = p * (dp - np.sum(p * dp, axis=1, keepdims=True))
+    return scale * (ds @ k), scale * (ds.T @ do), p.T @ do
+
+
+def _head_dv_not_transposed(q, k, v, do, scale):
+    dq, dk, _ = _ORIG_HEAD(q, k, v, do, scale)
+    p = _softmax(scale * (q @ k.T))
+    return dq, dk, (p.T @ do)[::-1]
+
+
+def _head_dp_uses_output(q, k, v, do, scale):
+    p = _softmax(scale * (q @ k.T))
+    dp = do @ (p @ v).T[:, : k.shape[0]] if q.shape[0] >= k.shape[0] else do @ v.T * 1.01
+    ds = p * (dp - np.sum(p * dp, axis=1, keepdims=True))
+    return scale * (ds @ k), scale * (ds.T @ q), p.T @ do
+
+
+BWD_MUTATIONS = {
+    "no_delta_term": _head_no_delta,
+    "delta_over_queries": _head_delta_wrong_axis,
+    "dq_missing_scale": _head_dq_unscaled,
+    "dk_from_dout": _head_dk_uses_keys,
+    "dv_rows_permuted": _head_dv_not_transposed,
+    "dp_perturbed": _head_dp_uses_output,
+}
+
+
+@pytest.mark.parametrize("name", sorted(BWD_MUTATIONS))
+def test_bwd_mutation_is_caught(name, monkeypatch):
+    monkeypatch.setattr(ob, "_one_head", BWD_MUTATIONS[name])
+    for check in pins.ALL_BWD_CHECKS:
+        try:
+            check(attn_bwd_ref, attn_ref)
+        except AssertionError:
+            return
+    raise AssertionError(name + " went unnoticed")

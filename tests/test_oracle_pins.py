@@ -55,3 +55,12 @@ def test_bf16_codec():
 @pytest.mark.parametrize("check", pins.ALL_NORM_CHECKS, ids=lambda c: c.__name__)
 def test_norm_pins(check):
     check(oracle.qk_norm_ref, oracle.RopeSpec)
+
+
+@pytest.mark.parametrize("check", pins.ALL_BWD_CHECKS, ids=lambda c: c.__name__)
+def test_bwd_pins(check):
+    check(oracle.attn_bwd_ref, oracle.attn_ref)
+
+
+def test_rope_transpose_pin():
+    pins.check_rope_transpose(oracle.rope_transpose_ref, oracle.rope3d_ref, oracle.RopeSpec)
