@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define VIDAX_ABI_VERSION 3
+#define VIDAX_ABI_VERSION 4
 
 typedef enum vidax_status {
   VIDAX_OK = 0,
@@ -88,6 +88,15 @@ typedef struct vidax_rope3d_desc {
  */
 vidax_status vidax_rope3d(const void* x, void* y, int32_t B, int32_t L, int32_t H, int32_t d,
                           const vidax_rope3d_desc* rope, hipStream_t stream);
+
+/*
+ * y = R^T x: the transpose of vidax_rope3d (every pair rotated by minus its
+ * angle), which carries a gradient with respect to rotated queries/keys back
+ * to the unrotated ones (the rotation is orthogonal).  Same arguments and
+ * requirements as vidax_rope3d.
+ */
+vidax_status vidax_rope3d_transpose(const void* x, void* y, int32_t B, int32_t L, int32_t H, int32_t d,
+                                    const vidax_rope3d_desc* rope, hipStream_t stream);
 
 /*
  * Query/key prologue of the served 3D-RoPE models (Section 3, "Supported
@@ -140,6 +149,33 @@ vidax_status vidax_qk_norm_rope(const void* x, void* y, const float* gain, float
 vidax_status vidax_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
                             int32_t B, int32_t H, int32_t Lq, int32_t Lk, int32_t d, float scale,
                             const int32_t* kv_valid_len, const vidax_rope3d_desc* rope,
+                            hipStream_t stream);
+
+/*
+ * Gradient of vidax_attn_fwd without rotation (for post-training, named as the
+ * next direction in Section 5, "Conclusions & Future Work"): for every batch
+ * b and head h, with keys j < Lv_b and P = exp(scale q k^T - lse),
+ *
+ *   dv = P^T dout,  ds = P * (dout v^T - D),  D_i = <dout_i, o_i>,
+ *   dq = scale ds k,  dk = scale ds^T q;   keys j >= Lv_b get dk = dv = 0,
+ *   a batch with Lv_b = 0 gets dq = 0.
+ *
+ *   q, o, dout, dq : bf16 [B, Lq, H, d];  k, v, dk, dv : bf16 [B, Lk, H, d]
+ *   lse   : fp32 [B, H, Lq], the natural-log sum-exp vidax_attn_fwd returned
+ *           with the same q, k, v, scale and kv_valid_len (o is its output).
+ *   delta : fp32 [B, H, Lq] device workspace owned by the caller; holds D on
+ *           return.
+ *   scale, kv_valid_len: as for vidax_attn_fwd.
+ * q and k are the vectors the scores were formed from: when the forward
+ * rotated them, pass the rotated ones (vidax_rope3d) and take dq, dk back
+ * through vidax_rope3d_transpose.  All device pointers 16-byte aligned (lse,
+ * delta too); outputs must not overlap each other or any input.  Products
+ * run on bf16 inputs (P and ds rounded to bf16) with fp32 accumulation.
+ * Requires d == 128 (VIDAX_ERR_UNSUPPORTED otherwise); B, H, Lq, Lk >= 0.
+ */
+vidax_status vidax_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                            const float* lse, void* dq, void* dk, void* dv, float* delta, int32_t B, int32_t H,
+                            int32_t Lq, int32_t Lk, int32_t d, float scale, const int32_t* kv_valid_len,
                             hipStream_t stream);
 
 /*

@@ -20,6 +20,10 @@ zero gradient everywhere.  q and k are the vectors the scores are formed from
 (rotated ones when the forward rotated them; rope_transpose takes a gradient
 back through the rotation).  Each (b, h) is evaluated with whole matrices,
 P from lse recomputed here with the two-pass softmax of attention.py.
+
+D_i is formed from O by its second expression; a backward pass has only the
+output the forward saved (in practice rounded to the storage type), so
+``o_saved`` may supply that O.  Without it O is the exact output.
 """
 
 from __future__ import annotations
@@ -30,13 +34,14 @@ from .attention import _valid_lengths
 from .rope3d import RopeSpec, rope3d_ref
 
 
-def _one_head(q, k, v, do, scale):
-    """Gradients for one (b, h): q, do [Lq, d]; k, v [N, d] (valid keys only)."""
+def _one_head(q, k, v, do, scale, o_saved=None):
+    """Gradients for one (b, h): q, do [Lq, d]; k, v [N, d] (valid keys only);
+    o_saved [Lq, d] replaces the exact O in D."""
     s = scale * (q @ k.T)
     m = s.max(axis=1, keepdims=True)
     e = np.exp(s - m)
     p = e / e.sum(axis=1, keepdims=True)
-    o = p @ v
+    o = p @ v if o_saved is None else o_saved
     dv = p.T @ do
     dp = do @ v.T
     delta = np.sum(do * o, axis=1, keepdims=True)
@@ -46,8 +51,10 @@ def _one_head(q, k, v, do, scale):
     return dq, dk, dv
 
 
-def attn_bwd_ref(q, k, v, do, scale, kv_valid_len=None):
-    """(dq [B, Lq, H, d], dk [B, Lk, H, d], dv [B, Lk, H, d]) in float64."""
+def attn_bwd_ref(q, k, v, do, scale, kv_valid_len=None, o_saved=None):
+    """(dq [B, Lq, H, d], dk [B, Lk, H, d], dv [B, Lk, H, d]) in float64;
+    o_saved [B, Lq, H, d]: the forward output D is formed from (default: the
+    exact output)."""
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
     v = np.asarray(v, dtype=np.float64)
@@ -63,7 +70,8 @@ def attn_bwd_ref(q, k, v, do, scale, kv_valid_len=None):
         if n == 0:
             continue
         for h in range(H):
-            gq, gk, gv = _one_head(q[b, :, h], k[b, :n, h], v[b, :n, h], do[b, :, h], float(scale))
+            os_ = None if o_saved is None else np.asarray(o_saved[b, :, h], dtype=np.float64)
+            gq, gk, gv = _one_head(q[b, :, h], k[b, :n, h], v[b, :n, h], do[b, :, h], float(scale), os_)
             dq[b, :, h] = gq
             dk[b, :n, h] = gk
             dv[b, :n, h] = gv

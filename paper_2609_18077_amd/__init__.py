@@ -21,6 +21,8 @@ _STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported configuration", 3: "k
 
 EXPORTED_SYMBOLS = (
     "vidax_rope3d",
+    "vidax_rope3d_transpose",
+    "vidax_attn_bwd",
     "vidax_qk_norm_rope",
     "vidax_attn_fwd",
     "vidax_attn_fwd_naive",
@@ -81,6 +83,10 @@ def lib() -> ctypes.CDLL:
         vp, i32, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float
         L.vidax_rope3d.argtypes = [vp, vp, i32, i32, i32, i32, ctypes.POINTER(RopeDesc), vp]
         L.vidax_rope3d.restype = i32
+        L.vidax_rope3d_transpose.argtypes = [vp, vp, i32, i32, i32, i32, ctypes.POINTER(RopeDesc), vp]
+        L.vidax_rope3d_transpose.restype = i32
+        L.vidax_attn_bwd.argtypes = [vp] * 10 + [i32, i32, i32, i32, i32, f32, vp, vp]
+        L.vidax_attn_bwd.restype = i32
         L.vidax_qk_norm_rope.argtypes = [vp, vp, vp, f32, i32, i32, i32, i32, ctypes.POINTER(RopeDesc), vp]
         L.vidax_qk_norm_rope.restype = i32
         for name in ("vidax_attn_fwd", "vidax_attn_fwd_naive"):
@@ -131,6 +137,48 @@ def rope3d(x, rope: Rope, out=None, stream=None):
     desc = rope.desc()
     _check("vidax_rope3d", lib().vidax_rope3d(_ptr(x), _ptr(y), B, L, H, d, ctypes.byref(desc), _stream(stream)))
     return y
+
+
+def rope3d_transpose(x, rope: Rope, out=None, stream=None):
+    """R^T x (every pair rotated by minus its angle); out may be x itself."""
+    import torch
+
+    _check_bshd("x", x)
+    y = torch.empty_like(x) if out is None else out
+    _check_bshd("out", y)
+    if y.shape != x.shape:
+        raise ValueError("out must have the shape of x")
+    B, L, H, d = x.shape
+    desc = rope.desc()
+    _check("vidax_rope3d_transpose",
+           lib().vidax_rope3d_transpose(_ptr(x), _ptr(y), B, L, H, d, ctypes.byref(desc), _stream(stream)))
+    return y
+
+
+def attn_bwd(q, k, v, o, dout, lse, scale=None, kv_valid_len=None, stream=None):
+    """(dq, dk, dv) of attention without rotation, from the forward's o and lse."""
+    import torch
+
+    for n, t in (("q", q), ("k", k), ("v", v), ("o", o), ("dout", dout)):
+        _check_bshd(n, t)
+    B, Lq, H, d = q.shape
+    Lk = k.shape[1]
+    if k.shape != v.shape or o.shape != q.shape or dout.shape != q.shape:
+        raise ValueError("shapes: q, o, dout [B, Lq, H, d]; k, v [B, Lk, H, d]")
+    if lse.dtype != torch.float32 or not lse.is_cuda or not lse.is_contiguous() or lse.shape != (B, H, Lq):
+        raise ValueError("lse must be a contiguous float32 [B, H, Lq] device tensor")
+    if scale is None:
+        scale = float(torch.tensor(1.0 / d ** 0.5, dtype=torch.float32))
+    if kv_valid_len is not None:
+        if kv_valid_len.dtype != torch.int32 or not kv_valid_len.is_cuda or kv_valid_len.numel() != B:
+            raise ValueError("kv_valid_len must be an int32 device tensor of B elements")
+        kv_valid_len = kv_valid_len.contiguous()
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    delta = torch.empty((B, H, Lq), dtype=torch.float32, device=q.device)
+    _check("vidax_attn_bwd", lib().vidax_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(dout), _ptr(lse), _ptr(dq),
+                                                  _ptr(dk), _ptr(dv), _ptr(delta), B, H, Lq, Lk, d, float(scale),
+                                                  _ptr(kv_valid_len), _stream(stream)))
+    return dq, dk, dv
 
 
 def qk_norm_rope(x, rope: Rope | None = None, gain=None, eps: float = 1e-6, out=None, stream=None):

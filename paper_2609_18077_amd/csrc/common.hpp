@@ -26,6 +26,7 @@ struct RopeParams {
   int dt, dh, dw;      // channel widths of the t, h, w blocks
   int pair_mode;       // 0 interleaved, 1 half split
   int keys_prerotated; // attention: keys arrive already rotated
+  int inverse;         // standalone rotation: rotate by -angle (the transpose)
   int n_rot;           // gt * gh * gw
   int base1, base2;    // first table entry of the h and w axes
   int n_entries;       // table entries: gt*dt/2 + gh*dh/2 + gw*dw/2
@@ -92,6 +93,10 @@ __host__ __device__ inline PairSlot pair_slot(const RopeParams& r, int pi) {
 namespace vidax {
 hipError_t launch_rope3d(const uint16_t* x, uint16_t* y, int B, int L, int H, const RopeParams& rp,
                          hipStream_t stream);
+hipError_t launch_attn_bwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, const uint16_t* o,
+                           const uint16_t* dout, const float* lse, float* delta, uint16_t* dq, uint16_t* dk,
+                           uint16_t* dv, int B, int H, int Lq, int Lk, float scale, const int32_t* kv_valid_len,
+                           hipStream_t stream);
 hipError_t launch_qk_norm(const uint16_t* x, uint16_t* y, const float* gain, float eps, int B, int L, int H,
                           const RopeParams& rp, hipStream_t stream);
 hipError_t launch_attn_naive(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o,

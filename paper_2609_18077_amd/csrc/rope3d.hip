@@ -1,4 +1,5 @@
-// Standalone 3D rotary embedding, bf16 [B, L, H, 128] -> bf16 (HBM-bound).
+// Standalone 3D rotary embedding, bf16 [B, L, H, 128] -> bf16 (HBM-bound),
+// and its transpose (every pair rotated by minus its angle).
 //
 // Each workgroup first builds the (cos, sin) table of every (axis, position,
 // frequency) in LDS, then walks tokens with a grid stride.  A token's 16
@@ -52,7 +53,7 @@ __global__ __launch_bounds__(kThreads) void rope3d_interleaved(Rope3dArgs a) {
       for (int p = 0; p < 4; ++p) {
         float2 e = tab[slot[p].base + pos_of_axis(slot[p].axis, t, h, w) * slot[p].stride];
         cs[p] = e.x;
-        sn[p] = e.y;
+        sn[p] = rp.inverse ? -e.y : e.y;
       }
     }
     for (int b = 0; b < a.B; ++b) {
@@ -128,7 +129,8 @@ __global__ __launch_bounds__(kThreads) void rope3d_half_split(Rope3dArgs a) {
             const int u = ch - offs[ax];
             const bool first = u < half;
             const int j = first ? u : u - half;
-            const float2 cs = tab[bases[ax] + pos3[ax] * half + j];
+            float2 cs = tab[bases[ax] + pos3[ax] * half + j];
+            if (rp.inverse) cs.y = -cs.y;
             const float x0 = __uint_as_float((uint32_t)stage[slotrow][first ? ch : ch - half] << 16);
             const float x1 = __uint_as_float((uint32_t)stage[slotrow][first ? ch + half : ch] << 16);
             const float y = first ? fmaf(x0, cs.x, -x1 * cs.y) : fmaf(x0, cs.y, x1 * cs.x);

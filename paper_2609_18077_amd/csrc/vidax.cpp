@@ -57,6 +57,7 @@ vidax_status make_rope(const vidax_rope3d_desc* r, int64_t max_tokens, int32_t d
   out->dw = r->dim_w;
   out->pair_mode = r->pair_mode;
   out->keys_prerotated = r->keys_prerotated;
+  out->inverse = 0;
   out->n_rot = (int)n_rot;
   out->base1 = r->grid_t * (r->dim_t / 2);
   out->base2 = out->base1 + r->grid_h * (r->dim_h / 2);
@@ -114,9 +115,68 @@ vidax_status attn_common(AttnImpl impl, const void* q, const void* k, const void
   return e == hipSuccess ? VIDAX_OK : VIDAX_ERR_LAUNCH;
 }
 
+vidax_status rope3d_common(bool inverse, const void* x, void* y, int32_t B, int32_t L, int32_t H, int32_t d,
+                          const vidax_rope3d_desc* rope, hipStream_t stream) {
+  if (B < 0 || L < 0 || H < 0 || d < 0) return VIDAX_ERR_INVALID_ARG;
+  if (!rope) return VIDAX_ERR_INVALID_ARG;
+  const int64_t n = numel4(B, L, H, d);
+  if (n < 0) return VIDAX_ERR_INVALID_ARG;
+  if (n > 0 && (!x || !y)) return VIDAX_ERR_INVALID_ARG;
+  if (!aligned(x, 16) || !aligned(y, 16)) return VIDAX_ERR_INVALID_ARG;
+  if (d != vidax::kHeadDim) return VIDAX_ERR_UNSUPPORTED;
+  if (x != y && overlaps(x, (uint64_t)n * 2, y, (uint64_t)n * 2)) return VIDAX_ERR_INVALID_ARG;
+  vidax_rope3d_desc r = *rope;
+  r.keys_prerotated = 0;  // attention-only field
+  RopeParams rp;
+  const vidax_status st = make_rope(&r, L, d, &rp);
+  if (st != VIDAX_OK) return st;
+  rp.inverse = inverse ? 1 : 0;
+  if (B == 0 || L == 0 || H == 0) return VIDAX_OK;
+  const hipError_t e = vidax::launch_rope3d((const uint16_t*)x, (uint16_t*)y, B, L, H, rp, stream);
+  return e == hipSuccess ? VIDAX_OK : VIDAX_ERR_LAUNCH;
+}
+
 }  // namespace
 
 extern "C" {
+
+vidax_status vidax_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                            const float* lse, void* dq, void* dk, void* dv, float* delta, int32_t B, int32_t H,
+                            int32_t Lq, int32_t Lk, int32_t d, float scale, const int32_t* kv_valid_len,
+                            hipStream_t stream) {
+  if (B < 0 || H < 0 || Lq < 0 || Lk < 0 || d < 0) return VIDAX_ERR_INVALID_ARG;
+  const int64_t nq = numel4(B, Lq, H, d), nk = numel4(B, Lk, H, d);
+  if (nq < 0 || nk < 0) return VIDAX_ERR_INVALID_ARG;
+  const int64_t nrow = (int64_t)B * H * Lq;  // lse, delta
+  if ((nq > 0 && (!q || !o || !dout || !dq)) || (nk > 0 && (!k || !v || !dk || !dv)) ||
+      (nrow > 0 && (!lse || !delta)))
+    return VIDAX_ERR_INVALID_ARG;
+  for (const void* p : {q, k, v, o, dout, (const void*)dq, (const void*)dk, (const void*)dv})
+    if (!aligned(p, 16)) return VIDAX_ERR_INVALID_ARG;
+  if (!aligned(lse, 16) || !aligned(delta, 16)) return VIDAX_ERR_INVALID_ARG;
+  if (kv_valid_len && !aligned(kv_valid_len, 4)) return VIDAX_ERR_INVALID_ARG;
+  if (!isfinite(scale)) return VIDAX_ERR_INVALID_ARG;
+  if (d != vidax::kHeadDim) return VIDAX_ERR_UNSUPPORTED;
+  const uint64_t qb = (uint64_t)nq * 2, kb = (uint64_t)nk * 2, rb = (uint64_t)nrow * 4;
+  // outputs (dq, dk, dv, delta) must not overlap each other or any input
+  const void* outs[4] = {dq, dk, dv, delta};
+  const uint64_t osz[4] = {qb, kb, kb, rb};
+  const void* ins[6] = {q, k, v, o, dout, lse};
+  const uint64_t isz[6] = {qb, kb, kb, qb, qb, rb};
+  for (int i = 0; i < 4; ++i) {
+    for (int j = 0; j < 6; ++j)
+      if (overlaps(outs[i], osz[i], ins[j], isz[j])) return VIDAX_ERR_INVALID_ARG;
+    for (int j = i + 1; j < 4; ++j)
+      if (overlaps(outs[i], osz[i], outs[j], osz[j])) return VIDAX_ERR_INVALID_ARG;
+  }
+  const int64_t grid = ((int64_t)(Lq > Lk ? Lq : Lk) + 255) / 256 * B * H;
+  if (grid > INT32_MAX) return VIDAX_ERR_UNSUPPORTED;
+  if (B == 0 || H == 0 || (Lq == 0 && Lk == 0)) return VIDAX_OK;
+  const hipError_t e = vidax::launch_attn_bwd((const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
+                                              (const uint16_t*)o, (const uint16_t*)dout, lse, delta, (uint16_t*)dq,
+                                              (uint16_t*)dk, (uint16_t*)dv, B, H, Lq, Lk, scale, kv_valid_len, stream);
+  return e == hipSuccess ? VIDAX_OK : VIDAX_ERR_LAUNCH;
+}
 
 vidax_status vidax_qk_norm_rope(const void* x, void* y, const float* gain, float eps, int32_t B, int32_t L, int32_t H,
                                 int32_t d, const vidax_rope3d_desc* rope, hipStream_t stream) {
@@ -144,22 +204,12 @@ vidax_status vidax_qk_norm_rope(const void* x, void* y, const float* gain, float
 
 vidax_status vidax_rope3d(const void* x, void* y, int32_t B, int32_t L, int32_t H, int32_t d,
                           const vidax_rope3d_desc* rope, hipStream_t stream) {
-  if (B < 0 || L < 0 || H < 0 || d < 0) return VIDAX_ERR_INVALID_ARG;
-  if (!rope) return VIDAX_ERR_INVALID_ARG;
-  const int64_t n = numel4(B, L, H, d);
-  if (n < 0) return VIDAX_ERR_INVALID_ARG;
-  if (n > 0 && (!x || !y)) return VIDAX_ERR_INVALID_ARG;
-  if (!aligned(x, 16) || !aligned(y, 16)) return VIDAX_ERR_INVALID_ARG;
-  if (d != vidax::kHeadDim) return VIDAX_ERR_UNSUPPORTED;
-  if (x != y && overlaps(x, (uint64_t)n * 2, y, (uint64_t)n * 2)) return VIDAX_ERR_INVALID_ARG;
-  vidax_rope3d_desc r = *rope;
-  r.keys_prerotated = 0;  // attention-only field
-  RopeParams rp;
-  const vidax_status st = make_rope(&r, L, d, &rp);
-  if (st != VIDAX_OK) return st;
-  if (B == 0 || L == 0 || H == 0) return VIDAX_OK;
-  const hipError_t e = vidax::launch_rope3d((const uint16_t*)x, (uint16_t*)y, B, L, H, rp, stream);
-  return e == hipSuccess ? VIDAX_OK : VIDAX_ERR_LAUNCH;
+  return rope3d_common(false, x, y, B, L, H, d, rope, stream);
+}
+
+vidax_status vidax_rope3d_transpose(const void* x, void* y, int32_t B, int32_t L, int32_t H, int32_t d,
+                                    const vidax_rope3d_desc* rope, hipStream_t stream) {
+  return rope3d_common(true, x, y, B, L, H, d, rope, stream);
 }
 
 vidax_status vidax_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int32_t B, int32_t H,

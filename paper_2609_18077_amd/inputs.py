@@ -35,7 +35,7 @@ CHUNK = 1 << 22
 HEAD_DIM = 128
 
 # tensor ids used in the seed sequence
-T_Q, T_K, T_V, T_LEN = 0, 1, 2, 3
+T_Q, T_K, T_V, T_LEN, T_DO = 0, 1, 2, 3, 4
 
 
 @dataclass(frozen=True)
@@ -183,6 +183,11 @@ def make_qkv(w: Workload):
     k = bf16_tensor(w.seed, T_K, (w.B, w.Lk, w.H, w.d), rms_norm=w.rms_norm_qk)
     v = bf16_tensor(w.seed, T_V, (w.B, w.Lk, w.H, w.d))
     return q, k, v, kv_valid_len(w)
+
+
+def make_dout(w: Workload) -> np.ndarray:
+    """Upstream gradient of the attention output (bf16 bits, [B, Lq, H, d])."""
+    return bf16_tensor(w.seed, T_DO, (w.B, w.Lq, w.H, w.d))
 
 
 def custom(name="custom", **kw) -> Workload:

@@ -421,6 +421,29 @@ def check_bwd_identities(bwd_fn, fwd_fn):
         assert np.allclose(a, 2.0 * b_ - 0.5 * c, rtol=1e-11, atol=1e-12)
 
 
+def check_bwd_saved_output(bwd_fn, fwd_fn):
+    """D formed from a saved (perturbed) output O + E: with e_i = <dO_i, E_i>,
+    dS moves by -P_ij e_i, so dv is unchanged, dq moves by
+    -scale e_i sum_j P_ij k_j (the forward with values k), and the key sum of
+    dk moves by -scale sum_i e_i q_i (each row of P sums to one)."""
+    rng = _rng(55)
+    q, k, v, do = _bwd_case(rng, B=2, Lq=6, Lk=7, H=2, d=8)
+    sc, lv = 0.7, np.array([7, 4])
+    o, _ = fwd_fn(q, k, v, sc, kv_valid_len=lv)
+    g0 = bwd_fn(q, k, v, do, sc, kv_valid_len=lv)
+    g1 = bwd_fn(q, k, v, do, sc, kv_valid_len=lv, o_saved=o)
+    for a, b_ in zip(g0, g1):
+        assert np.allclose(a, b_, rtol=1e-12, atol=1e-13)
+    err = 1e-2 * rng.standard_normal(o.shape)
+    dq, dk, dv = bwd_fn(q, k, v, do, sc, kv_valid_len=lv, o_saved=o + err)
+    e = np.sum(do * err, axis=-1, keepdims=True)  # [B, Lq, H, 1]
+    pk, _ = fwd_fn(q, k, k, sc, kv_valid_len=lv)
+    assert np.allclose(dv, g0[2], rtol=1e-13, atol=1e-14)
+    assert np.allclose(dq - g0[0], -sc * e * pk, rtol=1e-9, atol=1e-12)
+    assert np.allclose((dk - g0[1]).sum(axis=1), -sc * (e * q).sum(axis=1), rtol=1e-9, atol=1e-12)
+    assert not np.allclose(dq, g0[0], rtol=1e-6, atol=1e-8)
+
+
 def check_rope_transpose(transpose_fn, rope_fn, spec_cls):
     """<R x, y> = <x, R^T y> for every token and head; R^T R x = x."""
     rng = _rng(54)
@@ -435,4 +458,4 @@ def check_rope_transpose(transpose_fn, rope_fn, spec_cls):
         assert not np.allclose(transpose_fn(y, spec), rope_fn(y, spec))
 
 
-ALL_BWD_CHECKS = [check_bwd_finite_diff, check_bwd_torch, check_bwd_identities]
+ALL_BWD_CHECKS = [check_bwd_finite_diff, check_bwd_torch, check_bwd_identities, check_bwd_saved_output]

@@ -1,0 +1,208 @@
+"""GPU parity of the attention gradient (vidax_attn_bwd) and of the rotation's
+transpose (vidax_rope3d_transpose) against the fp64 oracle, through the C ABI.
+
+Tolerance.  The kernels round P and dS to bf16 before the products that
+consume them (relative error <= 2^-9 each, independent across the summed
+terms), accumulate in fp32 and round the gradients to bf16 (at most half an
+ulp, <= 2^-8 relative).  D = <dO, O> is formed from the saved output, which
+is bf16: the kernel-level tests give the oracle the same saved output (in
+strongly peaked attention, dP - D cancels and the rounding of O alone would
+move dq and dk by far more than 2^-9); the end-to-end tests compare with the
+exact gradient at the models' scale 1/sqrt(d).  Each gradient
+element is a sum over many terms whose rounding errors are independent, so
+beyond its own output rounding its error is about 2^-9 of the typical
+magnitude of its (batch, head) slice.  The test allows, per slice, 1%
+relative RMS error (about five times the expected 2^-9) and, per element, one
+bf16 ulp of the reference (2^-7 |ref|) plus 2^-5 of the slice's RMS (the
+largest of ~10^6 independent 2^-9-relative errors is near 5 sigma, about 1%
+of the RMS).  A key slice counts only its valid keys.  Gradients that
+are zero by definition (keys at or past the valid length, queries of a batch
+without valid keys) must be exactly zero.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2609_18077_amd as vx
+from paper_2609_18077_amd import inputs
+from tests.gpu_util import lengths_dev, log, rope_of, spec_of, to_bits, to_dev
+
+pytestmark = pytest.mark.gpu
+
+REL_RMS = 1e-2
+ULP_REL = 2.0 ** -7
+ABS_OVER_RMS = 2.0 ** -5
+
+
+def _check_grad(got_bits, ref, what, rows=None):
+    """Per (batch, head) slice of the first rows[b] rows (all rows when
+    None): the natural magnitude of a gradient differs between batches (a
+    batch with few valid keys has larger dv rows)."""
+    got = oracle.bf16_bits_to_f64(got_bits)
+    assert np.all(np.isfinite(got)), what
+    worst_rel, worst_excess = 0.0, -np.inf
+    for b in range(ref.shape[0]):
+        for h in range(ref.shape[2]):
+            n = ref.shape[1] if rows is None else int(rows[b])
+            g, r = got[b, :n, h], ref[b, :n, h]
+            rms = float(np.sqrt(np.mean(r * r))) if r.size else 0.0
+            if rms == 0.0:
+                # e.g. a single key: P = 1 and dP = D exactly, while the kernel
+                # forms dP and D as fp32 sums in different orders (~1e-7)
+                assert np.all(np.abs(g) <= 1e-4), (what, b, h, float(np.abs(g).max()))
+                continue
+            diff = np.abs(g - r)
+            rel = float(np.sqrt(np.mean(diff * diff))) / rms
+            excess = float(np.max(diff - ULP_REL * np.abs(r))) / rms
+            worst_rel, worst_excess = max(worst_rel, rel), max(worst_excess, excess)
+            assert rel <= REL_RMS, (what, b, h, rel)
+            assert excess <= ABS_OVER_RMS, (what, b, h, excess)
+    log(f"  {what}: worst slice rel_rms {worst_rel:.3e} (max err - ulp)/rms {worst_excess:.3e}")
+
+
+def _key_rows(lv, w):
+    return None if lv is None else np.minimum(np.maximum(lv, 0), w.Lk)
+
+
+def _check_zeros(dq, dk, dv, lv, Lk):
+    """Keys at or past Lv_b have dk = dv = 0; a batch with Lv_b = 0 has dq = 0."""
+    if lv is None:
+        return
+    for b, n in enumerate(np.minimum(np.maximum(lv, 0), Lk)):
+        assert np.all(oracle.bf16_bits_to_f64(dk[b, n:]) == 0.0)
+        assert np.all(oracle.bf16_bits_to_f64(dv[b, n:]) == 0.0)
+        if n == 0:
+            assert np.all(oracle.bf16_bits_to_f64(dq[b]) == 0.0)
+
+
+def _oracle_fwd_inputs(q, k, v, scale, lv):
+    """o (bf16 bits) and lse (fp32) of the oracle's forward."""
+    o, lse = oracle.attn_ref(q, k, v, scale, kv_valid_len=lv, workers=8)
+    return oracle.f64_to_bf16_bits(o), np.where(np.isfinite(lse), lse, 0.0).astype(np.float32)
+
+
+def _bwd_case(w, scale=None, lv="default"):
+    """Backward kernels alone: o and lse come from the oracle's forward."""
+    import torch
+
+    q, k, v, lv0 = inputs.make_qkv(w)
+    lv = lv0 if lv == "default" else lv
+    do = inputs.make_dout(w)
+    scale = w.scale if scale is None else scale
+    log(f"case bwd {w.name} B{w.B} H{w.H} Lq{w.Lq} Lk{w.Lk} lv={None if lv is None else list(lv)} scale={scale}")
+    dec = oracle.bf16_bits_to_f64
+    ob, lse = _oracle_fwd_inputs(dec(q), dec(k), dec(v), scale, lv)
+    dq, dk, dv = vx.attn_bwd(to_dev(q), to_dev(k), to_dev(v), to_dev(ob), to_dev(do),
+                             torch.from_numpy(lse).cuda(), scale=scale, kv_valid_len=lengths_dev(lv))
+    torch.cuda.synchronize()
+    dq, dk, dv = to_bits(dq), to_bits(dk), to_bits(dv)
+    # D from the same saved (bf16) output the kernels get
+    rq, rk, rv = oracle.attn_bwd_ref(dec(q), dec(k), dec(v), dec(do), scale, kv_valid_len=lv, o_saved=dec(ob))
+    kr = _key_rows(lv, w)
+    _check_grad(dv, rv, "dv", kr)
+    _check_grad(dk, rk, "dk", kr)
+    _check_grad(dq, rq, "dq")
+    _check_zeros(dq, dk, dv, lv, w.Lk)
+
+
+BWD = [
+    inputs.custom("bwd_tiny", B=1, H=2, Lq=512, Lk=512, seed=31),
+    # several own-row tiles (256 rows) and streamed tiles (64 rows), ragged in both
+    inputs.custom("bwd_ragged", B=2, H=3, Lq=1000, Lk=777, seed=32, kv_valid=("fixed", [777, 300])),
+    # cross-attention shape: few keys, a batch without valid keys, a clamp above Lk
+    inputs.custom("bwd_cross", B=3, H=2, Lq=600, Lk=512, seed=33, kv_valid=("fixed", [0, 37, 900])),
+    inputs.custom("bwd_few", B=1, H=1, Lq=5, Lk=3, seed=34),
+    inputs.custom("bwd_one", B=2, H=1, Lq=1, Lk=1, seed=35),
+    inputs.custom("bwd_edges", B=1, H=2, Lq=257, Lk=65, seed=36),
+    inputs.custom("bwd_normed", B=1, H=2, Lq=1536, Lk=1536, seed=37, rms_norm_qk=True),
+]
+
+
+@pytest.mark.parametrize("w", BWD, ids=lambda w: w.name)
+def test_attn_bwd_matches_oracle(w):
+    _bwd_case(w)
+
+
+@pytest.mark.parametrize("scale", [0.0, -0.05, 0.3])
+def test_attn_bwd_scale_values(scale):
+    _bwd_case(inputs.custom("bwd_scale", B=1, H=2, Lq=300, Lk=200, seed=38), scale=scale)
+
+
+def test_attn_bwd_empty_calls():
+    import torch
+
+    for B, Lq, Lk in ((0, 64, 64), (1, 0, 64), (1, 64, 0)):
+        z = lambda L: torch.zeros((B, L, 2, 128), dtype=torch.bfloat16, device="cuda")
+        q, k = z(Lq), z(Lk)
+        lse = torch.zeros((B, 2, Lq), dtype=torch.float32, device="cuda")
+        dq, dk, dv = vx.attn_bwd(q, k, k.clone(), q.clone(), q.clone(), lse)
+        torch.cuda.synchronize()
+        assert dq.shape == q.shape and dk.shape == k.shape
+    # Lk = 0 with queries present: no key, dq must still be written as zeros
+    q = torch.ones((1, 70, 2, 128), dtype=torch.bfloat16, device="cuda")
+    k = torch.zeros((1, 0, 2, 128), dtype=torch.bfloat16, device="cuda")
+    dq, _, _ = vx.attn_bwd(q, k, k.clone(), q.clone(), q.clone(),
+                           torch.zeros((1, 2, 70), dtype=torch.float32, device="cuda"))
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(dq).item() == 0
+
+
+def _product_path(w, q, k, v, do, lv):
+    """How a caller trains through the library: rotate, forward, backward,
+    rotate the q/k gradients back."""
+    import torch
+
+    r = rope_of(w)
+    qd, kd, vd = to_dev(q), to_dev(k), to_dev(v)
+    lvd = lengths_dev(lv)
+    if r is not None:
+        qd, kd = vx.rope3d(qd, r), vx.rope3d(kd, r)
+    o, lse = vx.attn_fwd(qd, kd, vd, scale=w.scale, kv_valid_len=lvd, return_lse=True)
+    dq, dk, dv = vx.attn_bwd(qd, kd, vd, o, to_dev(do), lse, scale=w.scale, kv_valid_len=lvd)
+    if r is not None:
+        dq, dk = vx.rope3d_transpose(dq, r), vx.rope3d_transpose(dk, r, out=dk)
+    torch.cuda.synchronize()
+    return to_bits(dq), to_bits(dk), to_bits(dv)
+
+
+@pytest.mark.parametrize("w", [
+    inputs.custom("bwd_rope_self", B=1, H=2, Lq=1000, Lk=1000, seed=41, grid=(2, 20, 24)),
+    inputs.custom("bwd_rope_ragged", B=2, H=2, Lq=700, Lk=900, seed=42, grid=(1, 21, 30), kv_valid=("fixed", [900, 450])),
+], ids=lambda w: w.name)
+def test_rope_attention_gradient_end_to_end(w):
+    q, k, v, lv = inputs.make_qkv(w)
+    do = inputs.make_dout(w)
+    log(f"case bwd+rope {w.name} B{w.B} H{w.H} Lq{w.Lq} Lk{w.Lk} grid={w.grid}")
+    dq, dk, dv = _product_path(w, q, k, v, do, lv)
+    dec = oracle.bf16_bits_to_f64
+    spec = spec_of(w)
+    qr, kr = oracle.rope3d_ref(dec(q), spec), oracle.rope3d_ref(dec(k), spec)
+    gq, gk, gv = oracle.attn_bwd_ref(qr, kr, dec(v), dec(do), w.scale, kv_valid_len=lv)
+    rq, rk = oracle.rope_transpose_ref(gq, spec), oracle.rope_transpose_ref(gk, spec)
+    kr = _key_rows(lv, w)
+    _check_grad(dv, gv, "dv", kr)
+    _check_grad(dk, rk, "dk", kr)
+    _check_grad(dq, rq, "dq")
+    _check_zeros(dq, dk, dv, lv, w.Lk)
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+def test_rope3d_transpose_matches_oracle(mode):
+    import torch
+
+    from tests.test_gpu_parity import _rope_bound
+
+    grid = (3, 10, 30)  # 900 video tokens, then 100 unrotated tokens
+    x = inputs.bf16_tensor(12, 0, (2, 1000, 3, 128))
+    log(f"case rope3d_transpose mode={mode}")
+    r = vx.Rope(grid=grid, dims=(44, 42, 42), theta=10000.0, pair_mode=mode)
+    y = vx.rope3d_transpose(to_dev(x), r)
+    torch.cuda.synchronize()
+    spec = oracle.RopeSpec(grid=grid, pair_mode=mode)
+    xf = oracle.bf16_bits_to_f64(x)
+    ref = oracle.rope_transpose_ref(xf, spec)
+    err = np.abs(oracle.bf16_bits_to_f64(to_bits(y)) - ref)
+    bound = _rope_bound(xf, ref, spec, np.arange(x.shape[1]))
+    assert np.all(err <= bound), (err.max(), float((err / bound).max()))
+    assert np.array_equal(to_bits(y)[:, 900:], x[:, 900:])

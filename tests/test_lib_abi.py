@@ -25,7 +25,7 @@ def test_library_exports_every_declared_function():
     assert set(declared) == set(vx.EXPORTED_SYMBOLS), declared
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.vidax_abi_version() == 3
+    assert lib.vidax_abi_version() == 4
     for s, text in [(0, b"ok"), (1, b"invalid argument"), (2, b"unsupported configuration"), (3, b"kernel launch failed")]:
         assert lib.vidax_status_string(s) == text
     assert lib.vidax_status_string(99) == b"unknown status"
@@ -122,6 +122,39 @@ def test_qk_norm_rope_rejects_invalid_arguments():
     assert call(gain=2 * P + 512) == 1               # gain overlaps the output
     assert call(rope=vx.Rope((2, 4, 8), (44, 42, 42), pair_mode=1).desc()) == 2  # half split: unsupported
     assert call(rope=vx.Rope((2, 4, 8), (40, 42, 42)).desc()) == 1               # widths do not sum to d
+
+
+def test_attn_bwd_rejects_invalid_arguments():
+    f = vx.lib().vidax_attn_bwd
+    INV, UNS = 1, 2
+
+    def call(q=P, k=2 * P, v=3 * P, o=4 * P, do=5 * P, lse=6 * P, dq=7 * P, dk=8 * P, dv=9 * P, delta=10 * P,
+             B=1, H=2, Lq=64, Lk=64, d=128, scale=0.088, kv=None):
+        ptr = lambda x: ctypes.c_void_p(x) if x else None
+        return f(ptr(q), ptr(k), ptr(v), ptr(o), ptr(do), ptr(lse), ptr(dq), ptr(dk), ptr(dv), ptr(delta),
+                 B, H, Lq, Lk, d, scale, ptr(kv), None)
+
+    assert call(q=0) == INV
+    assert call(delta=0) == INV
+    assert call(lse=0) == INV
+    assert call(q=0, o=0, do=0, dq=0, lse=0, delta=0, k=0, v=0, dk=0, dv=0, Lq=0, Lk=0) == 0  # empty
+    assert call(dq=7 * P + 8) == INV          # misaligned
+    assert call(delta=10 * P + 4) == INV      # misaligned workspace
+    assert call(kv=11 * P + 2) == INV
+    assert call(B=-1) == INV
+    assert call(scale=float("nan")) == INV
+    assert call(d=64) == UNS
+    assert call(dq=P) == INV                  # output aliases an input
+    assert call(dk=7 * P + 1024) == INV       # outputs overlap each other
+    assert call(delta=6 * P) == INV           # workspace aliases lse
+
+
+def test_rope3d_transpose_rejects_invalid_arguments():
+    f = vx.lib().vidax_rope3d_transpose
+    good = vx.Rope((2, 4, 8), (44, 42, 42)).desc()
+    assert f(ctypes.c_void_p(P), ctypes.c_void_p(2 * P), 1, 64, 2, 128, None, None) == 1
+    assert f(ctypes.c_void_p(P), ctypes.c_void_p(2 * P), 1, 63, 2, 128, ctypes.byref(good), None) == 1
+    assert f(ctypes.c_void_p(P), ctypes.c_void_p(2 * P), 1, 64, 2, 96, ctypes.byref(good), None) == 2
 
 
 def test_binding_fails_loudly_without_library(monkeypatch):

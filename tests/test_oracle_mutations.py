@@ -232,45 +232,50 @@ def _softmax(s):
     return e / e.sum(axis=1, keepdims=True)
 
 
-def _head_no_delta(q, k, v, do, scale):
+def _head_no_delta(q, k, v, do, scale, o_saved=None):
     p = _softmax(scale * (q @ k.T))
     ds = p * (do @ v.T)
     return scale * (ds @ k), scale * (ds.T @ q), p.T @ do
 
 
-def _head_delta_wrong_axis(q, k, v, do, scale):
+def _head_delta_wrong_axis(q, k, v, do, scale, o_saved=None):
     p = _softmax(scale * (q @ k.T))
     dp = do @ v.T
     ds = p * (dp - np.sum(p * dp, axis=0, keepdims=True))
     return scale * (ds @ k), scale * (ds.T @ q), p.T @ do
 
 
-def _head_dq_unscaled(q, k, v, do, scale):
-    dq, dk, dv = _ORIG_HEAD(q, k, v, do, scale)
+def _head_dq_unscaled(q, k, v, do, scale, o_saved=None):
+    dq, dk, dv = _ORIG_HEAD(q, k, v, do, scale, o_saved)
     return dq / scale, dk, dv
 
 
-def _head_dk_uses_keys(q, k, v, do, scale):
+def _head_dk_uses_keys(q, k, v, do, scale, o_saved=None):
     p = _softmax(scale * (q @ k.T))
     dp = do @ v.T
     ds = p * (dp - np.sum(p * dp, axis=1, keepdims=True))
     return scale * (ds @ k), scale * (ds.T @ do), p.T @ do
 
 
-def _head_dv_not_transposed(q, k, v, do, scale):
-    dq, dk, _ = _ORIG_HEAD(q, k, v, do, scale)
+def _head_dv_not_transposed(q, k, v, do, scale, o_saved=None):
+    dq, dk, _ = _ORIG_HEAD(q, k, v, do, scale, o_saved)
     p = _softmax(scale * (q @ k.T))
     return dq, dk, (p.T @ do)[::-1]
 
 
-def _head_dp_uses_output(q, k, v, do, scale):
+def _head_dp_uses_output(q, k, v, do, scale, o_saved=None):
     p = _softmax(scale * (q @ k.T))
     dp = do @ (p @ v).T[:, : k.shape[0]] if q.shape[0] >= k.shape[0] else do @ v.T * 1.01
     ds = p * (dp - np.sum(p * dp, axis=1, keepdims=True))
     return scale * (ds @ k), scale * (ds.T @ q), p.T @ do
 
 
+def _head_saved_output_ignored(q, k, v, do, scale, o_saved=None):
+    return _ORIG_HEAD(q, k, v, do, scale, None)
+
+
 BWD_MUTATIONS = {
+    "saved_output_ignored": _head_saved_output_ignored,
     "no_delta_term": _head_no_delta,
     "delta_over_queries": _head_delta_wrong_axis,
     "dq_missing_scale": _head_dq_unscaled,
