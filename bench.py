@@ -173,6 +173,40 @@ def time_prologues(w, steps):
     return out
 
 
+def time_backward(w, steps):
+    """vidax_attn_bwd (delta, dq, dk, dv kernels) on the workload's shape,
+    after a forward for o and lse; algorithmic flops are 2.5x the forward's
+    (S recomputed once, then dP, dV, dQ, dK: five products of 2 Lq Lv d)."""
+    import torch
+
+    import paper_2609_18077_amd as vx
+    from paper_2609_18077_amd import inputs
+
+    def up(a):
+        return torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
+
+    q, k, v, lv = inputs.make_qkv(w)
+    q, k, v, do = up(q), up(k), up(v), up(inputs.make_dout(w))
+    lvd = None if lv is None else torch.from_numpy(np.asarray(lv, dtype=np.int32)).cuda()
+    o, lse = vx.attn_fwd(q, k, v, scale=w.scale, kv_valid_len=lvd, return_lse=True)
+    fn = lambda: vx.attn_bwd(q, k, v, o, do, lse, scale=w.scale, kv_valid_len=lvd)
+    for _ in range(2):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    fl = 2.5 * flops(w, lv)
+    tf = fl / (ms * 1e-3) / 1e12
+    name = "attn_bwd_" + w.name
+    log(f"[bench] {name:28s} {ms:9.3f} ms  {tf:8.1f} TFLOP/s  {100 * tf / PEAK_BF16_TFLOPS:5.1f}% (algorithmic 2.5x fwd)")
+    return {name: {"ms": ms, "tflops": tf, "pct_bf16_peak": 100 * tf / PEAK_BF16_TFLOPS}}
+
+
 def cpu_baseline(w, q, k, v, lv, budget_s=12.0):
     """The fp64 oracle on a bounded sample: whole heads of the same workload,
     all query rows, one head at a time until the time budget is used."""
@@ -280,6 +314,9 @@ def main():
                 f"{rows[name]['pct_bf16_peak']:5.1f}%  {rows[name]['algorithmic_GBs']:8.1f} GB/s")
             torch.cuda.empty_cache()
         rows.update(time_prologues(inputs.WORKLOADS["wan13b_480p"], max(5, args.steps // 2)))
+        for name in ("wan13b_480p", "cross_text"):
+            rows.update(time_backward(inputs.WORKLOADS[name], max(5, args.steps // 2)))
+            torch.cuda.empty_cache()
         os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
         with open(os.path.join(ROOT, "gpurun_out", "bench_all.json"), "w") as f:
             json.dump(rows, f, indent=1)

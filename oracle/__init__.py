@@ -24,7 +24,7 @@ from .bf16 import bf16_bits_to_f64, f64_to_bf16_bits
 from .rope3d import RopeSpec, rope3d_ref, rope_angles
 from .attention import attn_ref, attn_ref_rows
 from .qknorm import qk_norm_ref
-from .attention_bwd import attn_bwd_ref, rope_transpose_ref
+from .attention_bwd import attn_bwd_ref, attn_bwd_ref_rows, rope_transpose_ref
 
 __all__ = [
     "bf16_bits_to_f64",
@@ -36,5 +36,6 @@ __all__ = [
     "attn_ref_rows",
     "qk_norm_ref",
     "attn_bwd_ref",
+    "attn_bwd_ref_rows",
     "rope_transpose_ref",
 ]

@@ -30,7 +30,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from .attention import _valid_lengths
+from .attention import _valid_lengths, attn_ref, attn_ref_rows
 from .rope3d import RopeSpec, rope3d_ref
 
 
@@ -75,6 +75,52 @@ def attn_bwd_ref(q, k, v, do, scale, kv_valid_len=None, o_saved=None):
             dq[b, :, h] = gq
             dk[b, :n, h] = gk
             dv[b, :n, h] = gv
+    return dq, dk, dv
+
+
+def attn_bwd_ref_rows(q, k, v, do, scale, q_rows, k_rows, kv_valid_len=None, workers: int = 1):
+    """Exact gradient at selected rows: dq at query rows q_rows [B, Rq, H, d],
+    dk and dv at key rows k_rows [B, Rk, H, d].  A dq row needs only its own
+    probabilities and output (the forward of those rows); a dk/dv row needs
+    every query's lse and D, which come from the full forward of attention.py
+    (O exact), computed only when k_rows is not empty.  P is taken from lse by
+    its definition, P_ij = exp(scale <q_i, k_j> - lse_i)."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    do = np.asarray(do, dtype=np.float64)
+    q_rows = np.asarray(q_rows, dtype=np.int64)
+    k_rows = np.asarray(k_rows, dtype=np.int64)
+    B, Lq, H, d = q.shape
+    Lk = k.shape[1]
+    lv = _valid_lengths(kv_valid_len, B, Lk)
+    oq, lq = attn_ref_rows(q, k, v, scale, q_rows, kv_valid_len=kv_valid_len, workers=workers)
+    if len(k_rows):
+        o, lse = attn_ref(q, k, v, scale, kv_valid_len=kv_valid_len, workers=workers)
+    dq = np.zeros((B, len(q_rows), H, d))
+    dk = np.zeros((B, len(k_rows), H, d))
+    dv = np.zeros((B, len(k_rows), H, d))
+    sc = float(scale)
+    for b in range(B):
+        n = lv[b]
+        if n == 0:
+            continue
+        for h in range(H):
+            K, V, Q, dO = k[b, :n, h], v[b, :n, h], q[b, :, h], do[b, :, h]
+            # query rows
+            dOr = dO[q_rows]
+            p = np.exp(sc * (Q[q_rows] @ K.T) - lq[b, h][:, None])
+            ds = p * (dOr @ V.T - np.sum(dOr * oq[b, :, h], axis=1)[:, None])
+            dq[b, :, h] = sc * (ds @ K)
+            # key rows (rows at or past n keep zero gradient)
+            live = k_rows < n
+            if live.any():
+                D = np.sum(dO * o[b, :, h], axis=1)  # [Lq]
+                kj, vj = K[k_rows[live]], V[k_rows[live]]
+                p = np.exp(sc * (Q @ kj.T) - lse[b, h][:, None])  # [Lq, R]
+                dv[b, live, h] = p.T @ dO
+                ds = p * (dO @ vj.T - D[:, None])
+                dk[b, live, h] = sc * (ds.T @ Q)
     return dq, dk, dv
 
 

@@ -206,3 +206,49 @@ def test_rope3d_transpose_matches_oracle(mode):
     bound = _rope_bound(xf, ref, spec, np.arange(x.shape[1]))
     assert np.all(err <= bound), (err.max(), float((err / bound).max()))
     assert np.array_equal(to_bits(y)[:, 900:], x[:, 900:])
+
+
+# ------------------------------------------------------------ full size ---
+
+def _edge_rows(L, rng, n=64):
+    return np.unique(np.r_[0, 1, 63, 64, 255, 256, L - 257, L - 256, L - 65, L - 64, L - 1,
+                           rng.integers(0, L, n)].clip(0, L - 1))
+
+
+@pytest.mark.parametrize("name,dkv_heads", [("wan13b_480p", [5]), ("cross_text", [0, 39])])
+def test_attn_bwd_full_size_sampled(name, dkv_heads):
+    """The benchmark's shape, sampled rows against the oracle's exact gradient
+    (D from the exact output): dq rows of every head (each needs only its own
+    row of P), dk/dv rows of a few heads (each needs the lse and D of every
+    query, a full forward of that head in the oracle)."""
+    import torch
+
+    w = inputs.WORKLOADS[name]
+    q, k, v, lv = inputs.make_qkv(w)
+    do = inputs.make_dout(w)
+    log(f"case bwd full {name} B{w.B} H{w.H} Lq{w.Lq} Lk{w.Lk}")
+    qd, kd, vd, lvd = to_dev(q), to_dev(k), to_dev(v), lengths_dev(lv)
+    o, lse = vx.attn_fwd(qd, kd, vd, scale=w.scale, kv_valid_len=lvd, return_lse=True)
+    dq, dk, dv = vx.attn_bwd(qd, kd, vd, o, to_dev(do), lse, scale=w.scale, kv_valid_len=lvd)
+    torch.cuda.synchronize()
+    del o, lse, qd, kd, vd
+    dq, dk, dv = to_bits(dq), to_bits(dk), to_bits(dv)
+    dec = oracle.bf16_bits_to_f64
+    rng = np.random.default_rng(7)
+    qrows, krows = _edge_rows(w.Lq, rng), _edge_rows(w.Lk, rng)
+    # dq rows of every head: rows are independent, so the oracle gets only them
+    nr = len(qrows)
+    rq, _, _ = oracle.attn_bwd_ref_rows(dec(q[:, qrows]), dec(k), dec(v), dec(do[:, qrows]), w.scale,
+                                        np.arange(nr), [], kv_valid_len=lv, workers=16)
+    _check_grad(dq[:, qrows], rq, "dq, every head")
+    # dk/dv rows of a few heads
+    hs = dkv_heads
+    _, rk, rv = oracle.attn_bwd_ref_rows(dec(q[:, :, hs]), dec(k[:, :, hs]), dec(v[:, :, hs]), dec(do[:, :, hs]),
+                                         w.scale, [], krows, kv_valid_len=lv, workers=16)
+    # krows is sorted: the valid keys of batch b are its first n[b] entries
+    n = None if lv is None else np.array([np.sum(krows < min(max(x, 0), w.Lk)) for x in lv])
+    _check_grad(dv[:, krows][:, :, hs], rv, f"dv heads {hs}", n)
+    _check_grad(dk[:, krows][:, :, hs], rk, f"dk heads {hs}", n)
+    for g in (dq, dk, dv):
+        assert np.all(np.isfinite(dec(g)))
+    _check_zeros(dq, dk, dv, lv, w.Lk)

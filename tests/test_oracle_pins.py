@@ -64,3 +64,27 @@ def test_bwd_pins(check):
 
 def test_rope_transpose_pin():
     pins.check_rope_transpose(oracle.rope_transpose_ref, oracle.rope3d_ref, oracle.RopeSpec)
+
+
+def _bwd_rows_all(q, k, v, do, scale, kv_valid_len=None):
+    return oracle.attn_bwd_ref_rows(q, k, v, do, scale, np.arange(q.shape[1]), np.arange(k.shape[1]),
+                                    kv_valid_len=kv_valid_len)
+
+
+@pytest.mark.parametrize("check", pins.ALL_BWD_CHECKS[:3], ids=lambda c: c.__name__)
+def test_bwd_rows_pins(check):
+    """The row-sampled gradient, asked for every row, meets the same pins."""
+    check(_bwd_rows_all, oracle.attn_ref)
+
+
+def test_bwd_rows_subset():
+    rng = np.random.default_rng(56)
+    q, k, v, do = (rng.standard_normal(s) for s in ((2, 11, 2, 8), (2, 9, 2, 8), (2, 9, 2, 8), (2, 11, 2, 8)))
+    lv = np.array([9, 4])
+    qr, kr = np.array([10, 0, 3]), np.array([8, 1, 5, 3])
+    dq, dk, dv = _bwd_rows_all(q, k, v, do, 0.4, kv_valid_len=lv)
+    sq, sk, sv = oracle.attn_bwd_ref_rows(q, k, v, do, 0.4, qr, kr, kv_valid_len=lv)
+    assert np.allclose(sq, dq[:, qr], rtol=1e-13, atol=1e-14)
+    assert np.allclose(sk, dk[:, kr], rtol=1e-13, atol=1e-14)
+    assert np.allclose(sv, dv[:, kr], rtol=1e-13, atol=1e-14)
+    assert np.all(sk[1, [0, 2]] == 0) and np.all(sv[1, [0, 2]] == 0)  # keys 8, 5 >= Lv = 4
