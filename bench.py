@@ -250,6 +250,8 @@ def main():
     ap.add_argument("--workload", default="wan13b_480p")
     ap.add_argument("--all", action="store_true", help="also time every workload (stderr + gpurun_out/bench_all.json)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--backward", action="store_true",
+                    help="only time vidax_attn_bwd on the workload (stderr) and exit (for profiling the backward)")
     ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
                     help="only run one plain device copy of MIB MiB (rocprofv3 counter calibration) and exit")
     args = ap.parse_args()
@@ -277,6 +279,9 @@ def main():
         return
 
     w = inputs.WORKLOADS[args.workload]
+    if args.backward:
+        time_backward(w, args.steps)
+        return
     r = time_gpu(w, args.steps, args.warmup)
     q, k, v, lv = r.pop("inputs")
     fl = flops(w, lv)
