@@ -16,8 +16,9 @@ method's arithmetic.
 
 ``qk_norm_ref`` is the query/key prologue that precedes the rotation in the
 served models (per-head RMS normalisation with a learned gain);
-``attn_bwd_ref`` is the gradient of the attention (for post-training), and
-``rope_transpose_ref`` carries a gradient back through the rotation.
+``attn_bwd_ref`` is the gradient of the attention (for post-training),
+``rope_transpose_ref`` carries a gradient back through the rotation, and
+``na3d_ref`` is the 3D neighbourhood (windowed) attention of a VAE decoder.
 """
 
 from .bf16 import bf16_bits_to_f64, f64_to_bf16_bits
@@ -25,6 +26,7 @@ from .rope3d import RopeSpec, rope3d_ref, rope_angles
 from .attention import attn_ref, attn_ref_rows
 from .qknorm import qk_norm_ref
 from .attention_bwd import attn_bwd_ref, attn_bwd_ref_rows, rope_transpose_ref
+from .na3d import na3d_ref
 
 __all__ = [
     "bf16_bits_to_f64",
@@ -38,4 +40,5 @@ __all__ = [
     "attn_bwd_ref",
     "attn_bwd_ref_rows",
     "rope_transpose_ref",
+    "na3d_ref",
 ]

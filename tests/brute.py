@@ -89,3 +89,40 @@ def qk_norm_row(x, gain, eps, n, rope):
         return y
     grid, dims, theta, mode = rope
     return rope_row(y, n, grid, dims, theta, mode)
+
+
+def _shift_start(c, N, K):
+    """Start of the K-position window holding c whose centre lies nearest to c
+    (found by trying every start)."""
+    r = (K - 1) // 2
+    return min(range(0, N - K + 1), key=lambda s: abs(s + r - c))
+
+
+def _in_window(c, cp, N, K, border):
+    """Does a key at axis position cp lie in the window of a query at c?"""
+    r = (K - 1) // 2
+    if border == "clip" or N <= K:
+        return abs(cp - c) <= r if border == "clip" else True
+    s = _shift_start(c, N, K)
+    return s <= cp < s + K
+
+
+def na3d(q, k, v, scale, grid, window, border):
+    """Neighbourhood attention by testing every (query, key) pair of the grid
+    (coordinates found by walking it).  q/k/v [B][L][H][d] nested lists.
+    Returns (o [B][L][H][d], lse [B][H][L])."""
+    B, L, H, d = len(q), len(q[0]), len(q[0][0]), len(q[0][0][0])
+    pos = [coords_by_walk(n, grid) for n in range(L)]
+    o = [[[[0.0] * d for _ in range(H)] for _ in range(L)] for _ in range(B)]
+    lse = [[[0.0] * L for _ in range(H)] for _ in range(B)]
+    for b in range(B):
+        for h in range(H):
+            for i in range(L):
+                keys = [j for j in range(L)
+                        if all(_in_window(pos[i][a], pos[j][a], grid[a], window[a], border) for a in range(3))]
+                e = [math.exp(scale * math.fsum(q[b][i][h][c] * k[b][j][h][c] for c in range(d))) for j in keys]
+                z = math.fsum(e)
+                for c in range(d):
+                    o[b][i][h][c] = math.fsum(ej * v[b][j][h][c] for ej, j in zip(e, keys)) / z
+                lse[b][h][i] = math.log(z)
+    return o, lse

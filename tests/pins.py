@@ -459,3 +459,65 @@ def check_rope_transpose(transpose_fn, rope_fn, spec_cls):
 
 
 ALL_BWD_CHECKS = [check_bwd_finite_diff, check_bwd_torch, check_bwd_identities, check_bwd_saved_output]
+
+
+# ------------------------------------------------ neighbourhood attention ---
+
+def _na_case(rng, grid, H=2, d=6, B=1):
+    L = grid[0] * grid[1] * grid[2]
+    return tuple(rng.standard_normal((B, L, H, d)) for _ in range(3))
+
+
+def check_na_brute(na_fn, attn_fn):
+    """Every row against the all-pairs brute force, both border readings,
+    asymmetric grids and windows (axis order and radius matter)."""
+    from tests import brute
+
+    rng = _rng(61)
+    for grid, window in (((3, 4, 5), (3, 3, 3)), ((2, 5, 6), (1, 3, 5)), ((4, 3, 7), (3, 1, 5))):
+        q, k, v = _na_case(rng, grid)
+        for border in ("clip", "shift"):
+            o, lse = na_fn(q, k, v, 0.7, grid, window, border)
+            bo, bl = brute.na3d(q.tolist(), k.tolist(), v.tolist(), 0.7, grid, window, border)
+            assert np.allclose(o, np.array(bo), rtol=1e-11, atol=1e-12), (grid, window, border)
+            assert np.allclose(lse, np.array(bl), rtol=1e-11, atol=1e-12), (grid, window, border)
+
+
+def check_na_full_window(na_fn, attn_fn):
+    """A window covering the whole grid is full attention (both readings)."""
+    rng = _rng(62)
+    grid = (2, 3, 4)
+    q, k, v = _na_case(rng, grid, H=3, d=8, B=2)
+    ref, rl = attn_fn(q, k, v, 0.5)
+    for border, window in (("clip", (3, 5, 7)), ("shift", (3, 3, 5)), ("clip", (5, 9, 11))):
+        o, lse = na_fn(q, k, v, 0.5, grid, window, border)
+        assert np.allclose(o, ref, rtol=1e-12, atol=1e-13), (border, window)
+        assert np.allclose(lse, rl, rtol=1e-12, atol=1e-13), (border, window)
+
+
+def check_na_single_key(na_fn, attn_fn):
+    """A 1 x 1 x 1 window: each query sees only its own token: o = v, lse = s."""
+    rng = _rng(63)
+    grid = (2, 3, 5)
+    q, k, v = _na_case(rng, grid)
+    for border in ("clip", "shift"):
+        o, lse = na_fn(q, k, v, 0.3, grid, (1, 1, 1), border)
+        assert np.allclose(o, v, rtol=1e-13, atol=1e-14)
+        assert np.allclose(lse, 0.3 * np.einsum("blhd,blhd->bhl", q, k), rtol=1e-12, atol=1e-13)
+
+
+def check_na_interior_agree(na_fn, attn_fn):
+    """Queries whose centred window lies inside the grid see the same keys in
+    both readings; near the border they differ."""
+    rng = _rng(64)
+    grid, window = (5, 6, 7), (3, 3, 5)
+    q, k, v = _na_case(rng, grid)
+    oc, _ = na_fn(q, k, v, 0.6, grid, window, "clip")
+    os_, _ = na_fn(q, k, v, 0.6, grid, window, "shift")
+    t, h, w = np.meshgrid(np.arange(5), np.arange(6), np.arange(7), indexing="ij")
+    inner = ((t >= 1) & (t <= 3) & (h >= 1) & (h <= 4) & (w >= 2) & (w <= 4)).ravel()
+    assert np.allclose(oc[:, inner], os_[:, inner], rtol=1e-13, atol=1e-14)
+    assert not np.allclose(oc[:, ~inner], os_[:, ~inner])
+
+
+ALL_NA_CHECKS = [check_na_brute, check_na_full_window, check_na_single_key, check_na_interior_agree]

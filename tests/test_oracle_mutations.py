@@ -294,3 +294,80 @@ def test_bwd_mutation_is_caught(name, monkeypatch):
         except AssertionError:
             return
     raise AssertionError(name + " went unnoticed")
+
+
+# ------------------------------------------------ neighbourhood attention ---
+
+import oracle.na3d as na  # noqa: E402
+
+_ORIG_AXIS = na.axis_window
+_ORIG_KEYS = na.window_keys
+_ORIG_NA = na.na3d_ref
+
+
+def _axis_radius_plus_one(c, N, K, border):
+    return _ORIG_AXIS(c, N, K + 2, border)
+
+
+def _axis_borders_swapped(c, N, K, border):
+    return _ORIG_AXIS(c, N, K, "shift" if border == "clip" else "clip")
+
+
+def _axis_shift_clamp_off(c, N, K, border):
+    if border == "shift" and N > K:
+        r = (K - 1) // 2
+        lo = min(max(c - r, 0), N - K + 1)
+        return lo, min(lo + K - 1, N - 1)
+    return _ORIG_AXIS(c, N, K, border)
+
+
+def _keys_axes_reversed(t, h, w, grid, window, border):
+    return _ORIG_KEYS(t, h, w, grid, tuple(reversed(window)), border)
+
+
+def _keys_flattened_w_major(t, h, w, grid, window, border):
+    T, Hp, Wp = grid
+    idx = _ORIG_KEYS(t, h, w, grid, window, border)
+    tt, rem = np.divmod(idx, Hp * Wp)
+    hh, ww = np.divmod(rem, Wp)
+    return np.minimum((ww * Hp + hh) * T + tt, T * Hp * Wp - 1)
+
+
+def _na_scale_dropped(q, k, v, scale, grid, window=(11, 11, 11), border="clip", rows=None, workers=1):
+    return _ORIG_NA(q, k, v, 1.0, grid, window, border, rows, workers)
+
+
+NA_AXIS_MUTATIONS = {
+    "radius_plus_one": _axis_radius_plus_one,
+    "borders_swapped": _axis_borders_swapped,
+    "shift_clamp_off_by_one": _axis_shift_clamp_off,
+}
+NA_KEYS_MUTATIONS = {
+    "window_axes_reversed": _keys_axes_reversed,
+    "keys_flattened_w_major": _keys_flattened_w_major,
+}
+
+
+def _na_caught(fn=None):
+    for check in pins.ALL_NA_CHECKS:
+        try:
+            check(fn or na.na3d_ref, attn_ref)
+        except AssertionError:
+            return True
+    return False
+
+
+@pytest.mark.parametrize("name", sorted(NA_AXIS_MUTATIONS))
+def test_na_axis_mutation_is_caught(name, monkeypatch):
+    monkeypatch.setattr(na, "axis_window", NA_AXIS_MUTATIONS[name])
+    assert _na_caught(), name + " went unnoticed"
+
+
+@pytest.mark.parametrize("name", sorted(NA_KEYS_MUTATIONS))
+def test_na_keys_mutation_is_caught(name, monkeypatch):
+    monkeypatch.setattr(na, "window_keys", NA_KEYS_MUTATIONS[name])
+    assert _na_caught(), name + " went unnoticed"
+
+
+def test_na_scale_dropped_is_caught():
+    assert _na_caught(_na_scale_dropped)

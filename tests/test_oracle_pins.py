@@ -88,3 +88,8 @@ def test_bwd_rows_subset():
     assert np.allclose(sk, dk[:, kr], rtol=1e-13, atol=1e-14)
     assert np.allclose(sv, dv[:, kr], rtol=1e-13, atol=1e-14)
     assert np.all(sk[1, [0, 2]] == 0) and np.all(sv[1, [0, 2]] == 0)  # keys 8, 5 >= Lv = 4
+
+
+@pytest.mark.parametrize("check", pins.ALL_NA_CHECKS, ids=lambda c: c.__name__)
+def test_na_pins(check):
+    check(oracle.na3d_ref, oracle.attn_ref)
