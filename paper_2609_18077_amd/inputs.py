@@ -190,6 +190,48 @@ def make_dout(w: Workload) -> np.ndarray:
     return bf16_tensor(w.seed, T_DO, (w.B, w.Lq, w.H, w.d))
 
 
+@dataclass(frozen=True)
+class NaWorkload:
+    """One neighbourhood-attention call: token grid, window, border reading."""
+
+    name: str
+    B: int
+    H: int
+    grid: tuple
+    seed: int
+    window: tuple = (11, 11, 11)
+    border: str = "clip"
+    d: int = HEAD_DIM
+    description: str = field(default="", compare=False)
+
+    @property
+    def L(self) -> int:
+        return self.grid[0] * self.grid[1] * self.grid[2]
+
+    @property
+    def scale(self) -> float:
+        return float(np.float32(1.0 / np.sqrt(self.d)))
+
+
+# The paper names the LTX-2.5 VAE decoder's 11 x 11 x 11 neighbourhood
+# attention but not its shapes: the stand-in is a decoder stage at 1/16 of
+# 1280 x 720 (80 x 45 positions) over 16 latent frames, 512 channels as 4
+# heads of 128.
+NA_WORKLOADS = {
+    w.name: w
+    for w in [
+        NaWorkload("ltx_vae_na", B=1, H=4, grid=(16, 45, 80), seed=6,
+                   description="VAE-decoder neighbourhood attention, grid 16x45x80, window 11^3"),
+    ]
+}
+
+
+def make_na_qkv(w: NaWorkload):
+    """(q, k, v) uint16 bf16 bits [B, L, H, d] of a neighbourhood-attention workload."""
+    shape = (w.B, w.L, w.H, w.d)
+    return tuple(bf16_tensor(w.seed, t, shape) for t in (T_Q, T_K, T_V))
+
+
 def custom(name="custom", **kw) -> Workload:
     """A workload with explicit fields (used for parity cases between the named ones)."""
     return Workload(name=name, **kw)

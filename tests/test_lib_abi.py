@@ -25,7 +25,7 @@ def test_library_exports_every_declared_function():
     assert set(declared) == set(vx.EXPORTED_SYMBOLS), declared
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.vidax_abi_version() == 4
+    assert lib.vidax_abi_version() == 5
     for s, text in [(0, b"ok"), (1, b"invalid argument"), (2, b"unsupported configuration"), (3, b"kernel launch failed")]:
         assert lib.vidax_status_string(s) == text
     assert lib.vidax_status_string(99) == b"unknown status"
@@ -155,6 +155,38 @@ def test_rope3d_transpose_rejects_invalid_arguments():
     assert f(ctypes.c_void_p(P), ctypes.c_void_p(2 * P), 1, 64, 2, 128, None, None) == 1
     assert f(ctypes.c_void_p(P), ctypes.c_void_p(2 * P), 1, 63, 2, 128, ctypes.byref(good), None) == 1
     assert f(ctypes.c_void_p(P), ctypes.c_void_p(2 * P), 1, 64, 2, 96, ctypes.byref(good), None) == 2
+
+
+def test_na3d_rejects_invalid_arguments():
+    f = vx.lib().vidax_na3d_fwd
+    ws = vx.lib().vidax_na3d_workspace_bytes
+    INV, UNS = 1, 2
+    need = ws(1, 2, 3, 5, 7)
+    assert need == 1 * 2 * 128 * 3 * 5 * 8 * 2
+    assert ws(-1, 2, 3, 5, 7) == -1
+
+    def call(q=P, k=2 * P, v=3 * P, o=4 * P, lse=5 * P, w=6 * P, wb=need, B=1, H=2, g=(3, 5, 7), d=128,
+             win=(3, 3, 3), border=0, scale=0.088):
+        ptr = lambda x: ctypes.c_void_p(x) if x else None
+        return f(ptr(q), ptr(k), ptr(v), ptr(o), ptr(lse), ptr(w), wb, B, H, *g, d, *win, border, scale, None)
+
+    assert call(win=(2, 3, 3)) == INV       # even window
+    assert call(win=(3, 0, 3)) == INV
+    assert call(border=2) == INV
+    assert call(scale=float("inf")) == INV
+    assert call(q=0) == INV
+    assert call(w=0) == INV
+    assert call(wb=need - 2) == INV         # workspace too small
+    assert call(o=4 * P + 8) == INV         # misaligned
+    assert call(w=6 * P + 4) == INV
+    assert call(lse=5 * P + 2) == INV
+    assert call(d=64) == UNS
+    assert call(win=(3, 3, 13)) == UNS      # w window beyond one 16-key run
+    assert call(o=P) == INV                 # output aliases q
+    assert call(w=3 * P) == INV             # workspace aliases v
+    assert call(w=4 * P + 1024) == INV      # workspace overlaps o
+    assert call(B=0, q=0, k=0, v=0, o=0, lse=0, w=0, wb=0) == 0  # empty
+    assert call(g=(0, 5, 7), q=0, k=0, v=0, o=0, w=0, wb=0) == 0
 
 
 def test_binding_fails_loudly_without_library(monkeypatch):
