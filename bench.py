@@ -207,6 +207,51 @@ def time_backward(w, steps):
     return {name: {"ms": ms, "tflops": tf, "pct_bf16_peak": 100 * tf / PEAK_BF16_TFLOPS}}
 
 
+def na3d_pairs(w):
+    """(query, key) pairs of a neighbourhood-attention workload: the window
+    is a box, so the count is the product over the axes of the summed
+    per-position window lengths."""
+    n = 1
+    for N, K in zip(w.grid, w.window):
+        r = (K - 1) // 2
+        tot = 0
+        for c in range(N):
+            if w.border == "clip":
+                tot += min(N - 1, c + r) - max(0, c - r) + 1
+            else:
+                tot += min(N, K)
+        n *= tot
+    return n * w.B * w.H
+
+
+def time_na3d(w, steps):
+    """vidax_na3d_fwd on a neighbourhood-attention workload; algorithmic
+    FLOPs = 4 d per (query, window key) pair."""
+    import torch
+
+    import paper_2609_18077_amd as vx
+    from paper_2609_18077_amd import inputs
+
+    q, k, v = (torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16) for x in inputs.make_na_qkv(w))
+    o = torch.empty_like(q)
+    fn = lambda: vx.na3d_fwd(q, k, v, w.grid, w.window, w.border, scale=w.scale, out=o)
+    for _ in range(3):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    fl = 4.0 * w.d * na3d_pairs(w)
+    tf = fl / (ms * 1e-3) / 1e12
+    name = "na3d_" + w.name
+    log(f"[bench] {name:28s} {ms:9.3f} ms  {tf:8.1f} TFLOP/s  {100 * tf / PEAK_BF16_TFLOPS:5.1f}% (window pairs only)")
+    return {name: {"ms": ms, "tflops": tf, "pct_bf16_peak": 100 * tf / PEAK_BF16_TFLOPS, "pairs": na3d_pairs(w)}}
+
+
 def cpu_baseline(w, q, k, v, lv, budget_s=12.0):
     """The fp64 oracle on a bounded sample: whole heads of the same workload,
     all query rows, one head at a time until the time budget is used."""
@@ -252,6 +297,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--backward", action="store_true",
                     help="only time vidax_attn_bwd on the workload (stderr) and exit (for profiling the backward)")
+    ap.add_argument("--na", action="store_true",
+                    help="only time vidax_na3d_fwd on the neighbourhood-attention workloads (stderr) and exit")
     ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
                     help="only run one plain device copy of MIB MiB (rocprofv3 counter calibration) and exit")
     args = ap.parse_args()
@@ -281,6 +328,10 @@ def main():
     w = inputs.WORKLOADS[args.workload]
     if args.backward:
         time_backward(w, args.steps)
+        return
+    if args.na:
+        for ww in inputs.NA_WORKLOADS.values():
+            time_na3d(ww, args.steps)
         return
     r = time_gpu(w, args.steps, args.warmup)
     q, k, v, lv = r.pop("inputs")
@@ -322,6 +373,8 @@ def main():
         for name in ("wan13b_480p", "cross_text"):
             rows.update(time_backward(inputs.WORKLOADS[name], max(5, args.steps // 2)))
             torch.cuda.empty_cache()
+        for ww in inputs.NA_WORKLOADS.values():
+            rows.update(time_na3d(ww, max(10, args.steps)))
         os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
         with open(os.path.join(ROOT, "gpurun_out", "bench_all.json"), "w") as f:
             json.dump(rows, f, indent=1)

@@ -179,13 +179,6 @@ vidax_status vidax_attn_bwd(const void* q, const void* k, const void* v, const v
                             hipStream_t stream);
 
 /*
- * Bytes of the workspace vidax_na3d_fwd needs: B * H * 128 * grid_t * grid_h
- * * round_up(grid_w, 8) * 2 (a transposed copy of v).  -1 for negative sizes
- * or an overflow.
- */
-int64_t vidax_na3d_workspace_bytes(int32_t B, int32_t H, int32_t grid_t, int32_t grid_h, int32_t grid_w);
-
-/*
  * 3D neighbourhood (windowed) attention, the attention of the LTX-2.5 VAE
  * decoder (Section 2, "3D RoPE, 3D VAEs, and flash attention"; porting-bug
  * table, "Memory, Tiling & Execution Graphs"): on a token grid of
@@ -201,21 +194,17 @@ int64_t vidax_na3d_workspace_bytes(int32_t B, int32_t H, int32_t grid_t, int32_t
  *   natural-log sum-exp.
  *
  *   q, k, v, o : bf16 [B, L, H, d] device pointers, 16-byte aligned
- *   lse        : fp32 [B, H, L] device pointer or NULL
- *   workspace  : caller-owned device buffer of workspace_bytes >=
- *                vidax_na3d_workspace_bytes(B, H, grid_t, grid_h, grid_w),
- *                16-byte aligned; overwritten (a transposed copy of v)
+ *   lse        : fp32 [B, H, L] device pointer (4-byte aligned) or NULL
  *   win_t, win_h, win_w: odd >= 1 (VIDAX_ERR_INVALID_ARG otherwise);
  *                win_w <= 11 (VIDAX_ERR_UNSUPPORTED beyond)
  *   scale: finite.  Requires d == 128 (VIDAX_ERR_UNSUPPORTED otherwise).
- * o, lse and the workspace must not overlap each other or q, k, v.  Scores
+ * o and lse must not overlap each other or q, k, v.  Scores
  * are fp32 sums of bf16 products; the probabilities are rounded to bf16
  * before the product with v, as in vidax_attn_fwd.
  */
-vidax_status vidax_na3d_fwd(const void* q, const void* k, const void* v, void* o, float* lse, void* workspace,
-                            int64_t workspace_bytes, int32_t B, int32_t H, int32_t grid_t, int32_t grid_h,
-                            int32_t grid_w, int32_t d, int32_t win_t, int32_t win_h, int32_t win_w, int32_t border,
-                            float scale, hipStream_t stream);
+vidax_status vidax_na3d_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int32_t B, int32_t H,
+                            int32_t grid_t, int32_t grid_h, int32_t grid_w, int32_t d, int32_t win_t, int32_t win_h,
+                            int32_t win_w, int32_t border, float scale, hipStream_t stream);
 
 /*
  * Same contract as vidax_attn_fwd, computed by a plain scalar fp32 kernel (one

@@ -24,7 +24,6 @@ EXPORTED_SYMBOLS = (
     "vidax_rope3d_transpose",
     "vidax_attn_bwd",
     "vidax_na3d_fwd",
-    "vidax_na3d_workspace_bytes",
     "vidax_qk_norm_rope",
     "vidax_attn_fwd",
     "vidax_attn_fwd_naive",
@@ -89,9 +88,7 @@ def lib() -> ctypes.CDLL:
         L.vidax_rope3d_transpose.restype = i32
         L.vidax_attn_bwd.argtypes = [vp] * 10 + [i32, i32, i32, i32, i32, f32, vp, vp]
         L.vidax_attn_bwd.restype = i32
-        L.vidax_na3d_workspace_bytes.argtypes = [i32] * 5
-        L.vidax_na3d_workspace_bytes.restype = ctypes.c_int64
-        L.vidax_na3d_fwd.argtypes = [vp] * 6 + [ctypes.c_int64] + [i32] * 10 + [f32, vp]
+        L.vidax_na3d_fwd.argtypes = [vp] * 5 + [i32] * 10 + [f32, vp]
         L.vidax_na3d_fwd.restype = i32
         L.vidax_qk_norm_rope.argtypes = [vp, vp, vp, f32, i32, i32, i32, i32, ctypes.POINTER(RopeDesc), vp]
         L.vidax_qk_norm_rope.restype = i32
@@ -188,11 +185,9 @@ def attn_bwd(q, k, v, o, dout, lse, scale=None, kv_valid_len=None, stream=None):
 
 
 def na3d_fwd(q, k, v, grid, window=(11, 11, 11), border: str = "clip", scale=None, return_lse=False, out=None,
-             workspace=None, stream=None):
+             stream=None):
     """3D neighbourhood attention on a token grid (T, Hp, Wp); q, k, v bf16
-    [B, T*Hp*Wp, H, d].  border "clip" or "shift".  workspace: optional uint8
-    device tensor of at least na3d_workspace_bytes(...) bytes (allocated here
-    when None)."""
+    [B, T*Hp*Wp, H, d].  border "clip" or "shift"."""
     import torch
 
     for n, t in (("q", q), ("k", k), ("v", v)):
@@ -207,16 +202,10 @@ def na3d_fwd(q, k, v, grid, window=(11, 11, 11), border: str = "clip", scale=Non
         raise ValueError("border must be 'clip' or 'shift'")
     if scale is None:
         scale = float(torch.tensor(1.0 / d ** 0.5, dtype=torch.float32))
-    need = lib().vidax_na3d_workspace_bytes(B, H, T, Hp, Wp)
-    if need < 0:
-        raise ValueError("sizes out of range")
-    if workspace is None:
-        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
     o = torch.empty_like(q) if out is None else out
     _check_bshd("out", o)
     lse = torch.empty((B, H, L), dtype=torch.float32, device=q.device) if return_lse else None
-    _check("vidax_na3d_fwd", lib().vidax_na3d_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(workspace),
-                                                  workspace.numel() * workspace.element_size(), B, H, T, Hp, Wp, d,
+    _check("vidax_na3d_fwd", lib().vidax_na3d_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, H, T, Hp, Wp, d,
                                                   *(int(x) for x in window), 0 if border == "clip" else 1,
                                                   float(scale), _stream(stream)))
     return (o, lse) if return_lse else o

@@ -103,11 +103,9 @@ hipError_t launch_attn_naive(const uint16_t* q, const uint16_t* k, const uint16_
                              float* lse, int B, int H, int Lq, int Lk, float scale,
                              const int32_t* kv_valid_len, const RopeParams& rp, hipStream_t stream);
 bool attn_rope_supported(const RopeParams& rp);
-// Elements of the transposed-V workspace of the neighbourhood attention.
-size_t na3d_workspace_elems(int B, int H, int T, int Hp, int Wp);
-hipError_t launch_na3d_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o, float* lse,
-                           uint16_t* vt, int B, int H, int T, int Hp, int Wp, int kt, int kh, int kw, int shift,
-                           float scale, hipStream_t stream);
+hipError_t launch_na3d_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o, float* lse, int B,
+                           int H, int T, int Hp, int Wp, int kt, int kh, int kw, int shift, float scale,
+                           hipStream_t stream);
 hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o,
                            float* lse, int B, int H, int Lq, int Lk, float scale,
                            const int32_t* kv_valid_len, const RopeParams& rp, hipStream_t stream);

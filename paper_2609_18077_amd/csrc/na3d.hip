@@ -5,24 +5,29 @@
 // moved inward at the border), with a softmax over that key set.  bf16 in/out,
 // fp32 accumulation, head dim 128.
 //
-// One wave owns a 2 x 4 x 4 block of 32 queries (t, h, w).  The union of
-// their windows is a box of at most (kt + 1) x (kh + 3) x (kw + 3) keys; the
-// wave walks it as runs of 16 keys along w (one run per (t', h') row of the
-// box, starting at an even w), two runs per 32-key score block:
+// A workgroup of 8 waves owns a 2 x 8 x 16 block of queries (t, h, w); wave
+// (i, j) owns the 2 x 4 x 4 sub-block at h offset 4 i, w offset 4 j, 32
+// queries.  The union of the workgroup's windows is a box of rows (t', h')
+// times at most 26 consecutive w.  The workgroup streams that box two rows at
+// a time: each step copies the two rows' keys and values (32 w positions
+// each, from an even start) straight from global memory into LDS, double
+// buffered, one barrier per step.  A wave whose own key box contains either
+// row computes one 32-key score block from them -- 16 keys of each row, at
+// the wave's own offset along w -- as in the dense forward kernel:
 //
 //   S^T [32 keys x 32 queries] = K Q^T     8 x v_mfma_f32_32x32x16_bf16
 //   P^T = exp2(S^T c - m), zero outside each query's window
 //   O^T [128 x 32] += V^T P^T              8 x v_mfma_f32_32x32x16_bf16
 //
-// as in the dense forward kernel (score tile transposed so that a lane holds
-// one query; P taken from the accumulator layout as the B operand; the
+// (score tile transposed so that a lane holds one query; P taken from the
+// accumulator layout as the B operand; V^T read by ds_read_b64_tr_b16; the
 // softmax reference m reset only when a block's row sum leaves [0, 2^64)).
-// Waves are independent (no LDS, no barriers): the K operand is read straight
-// from global memory (a lane's 16 bytes are one key row's d-chunk), and the
-// V^T operand from a transposed copy of V written by the first launch,
-// [B, H, 128, T*Hp, Wps] with the w rows padded with zeros to Wps (a multiple
-// of 8), so a lane's 4 consecutive keys of one channel are one aligned 8-byte
-// load.  Out-of-range rows read as zero through buffer resources.
+// LDS holds the staged keys row-major, 256 bytes a key, with the 16-byte
+// chunk c of key x stored at chunk c ^ f(x mod 16), f(x) = 4 (x mod 4) +
+// x / 4: any 16 consecutive keys put one chunk in 16 different places (the
+// score reads), and any 4 consecutive keys put a 64-byte span in 4 different
+// quarters of the banks (the transposing reads).  Each 1 KB direct copy
+// fills 4 whole keys, 256 contiguous bytes of global memory each.
 #include "common.hpp"
 
 namespace vidax {
@@ -30,30 +35,31 @@ namespace {
 
 constexpr int D = kHeadDim;
 constexpr int QT = 2, QH = 4, QW = 4;  // query block of one wave
-constexpr int NWV = 4;                 // waves per workgroup
+constexpr int WH = 2, WW = 4;          // waves of a workgroup along h and w
+constexpr int NW = WH * WW, NT = NW * 64;
+constexpr int ROWK = 32;               // staged keys per row
+constexpr int STEPK = 2 * ROWK;        // keys per step (two rows)
+constexpr int BUF = STEPK * D;         // elements of one staged tensor
 constexpr int kBufferFlags = 0x00020000;  // raw buffer, 32-bit data format
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kSumLimit = 18446744073709551616.0f;  // 2^64
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void* lds_ptr;
 
 struct NaArgs {
   const uint16_t* q;
   const uint16_t* k;
-  const uint16_t* vt;
+  const uint16_t* v;
   uint16_t* o;
   float* lse;
   int B, H, T, Hp, Wp, L;
-  int Wps;    // padded row length of the transposed V
-  int plane;  // T * Hp * Wps: elements of one channel of one (b, h) in vt
   int kt, kh, kw;
   int shift;       // border: 0 clip, 1 shift
   float c;         // |scale| log2(e)
   uint32_t qsign;  // 0x80008000 when scale < 0: queries enter negated
-  int nbt, nbh, nbw;
-  int nblk;  // wave blocks: B * H * nbt * nbh * nbw
+  int nbt, nbh, nbw;  // workgroup blocks per axis
   int nwg;
 };
 
@@ -76,6 +82,10 @@ __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c, false);
 }
 
+__device__ __forceinline__ i16x4 lds_read_tr16(const uint16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p));
+}
+
 // Inclusive window [lo, hi] on an axis of N positions for a query at c
 // (window size K odd): clipped to the axis, or moved inward to keep K.
 __device__ __forceinline__ int2 axis_window(int c, int N, int K, int shift) {
@@ -86,60 +96,23 @@ __device__ __forceinline__ int2 axis_window(int c, int N, int K, int shift) {
   return make_int2(lo, lo + K - 1);
 }
 
-// ---- vt[b][h][c][row][w] = v[b][row * Wp + w][h][c] (rows = T * Hp), zero
-// for Wp <= w < Wps.  Workgroup: one (b, h, row) and 64 positions of w.
-__global__ __launch_bounds__(256) void na3d_transpose_v_kernel(const uint16_t* __restrict__ v,
-                                                               uint16_t* __restrict__ vt, NaArgs a) {
-  __shared__ uint16_t tile[64][D + 8];
-  const int nwc = (a.Wps + 63) >> 6;
-  int x = blockIdx.x;
-  const int wc = x % nwc;
-  x /= nwc;
-  const int row = x % (a.T * a.Hp);
-  x /= a.T * a.Hp;
-  const int h = x % a.H, b = x / a.H;
-  const int w0 = wc * 64;
-  const int tid = threadIdx.x;
-  const size_t tok = (size_t)a.H * D;
-  // load 64 tokens x 128 channels, 16 bytes per thread and pass
-#pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    const int e = p * 256 + tid;  // chunk index: token e >> 4, chunk e & 15
-    const int wl = e >> 4, ch = e & 15;
-    const int w = w0 + wl;
-    uint4 val = make_uint4(0, 0, 0, 0);
-    if (w < a.Wp) val = *reinterpret_cast<const uint4*>(v + ((size_t)b * a.L + (size_t)row * a.Wp + w) * tok + (size_t)h * D + ch * 8);
-    *reinterpret_cast<uint4*>(&tile[wl][ch * 8]) = val;
-  }
-  __syncthreads();
-  // write 128 channels x 64 positions, 4 positions (8 bytes) per thread and pass
-  uint16_t* out = vt + ((size_t)b * a.H + h) * D * a.plane + (size_t)row * a.Wps;
-#pragma unroll
-  for (int p = 0; p < 8; ++p) {
-    const int e = p * 256 + tid;  // channel e >> 4, positions 4 (e & 15) ..
-    const int c = e >> 4, wl = 4 * (e & 15);
-    if (w0 + wl < a.Wps) {  // Wps is a multiple of 8: all four positions are in the row
-      uint2 pk;
-      pk.x = (uint32_t)tile[wl][c] | ((uint32_t)tile[wl + 1][c] << 16);
-      pk.y = (uint32_t)tile[wl + 2][c] | ((uint32_t)tile[wl + 3][c] << 16);
-      *reinterpret_cast<uint2*>(out + (size_t)c * a.plane + w0 + wl) = pk;
-    }
-  }
+// 16-byte chunk slot of chunk c of staged key x (an involution in c)
+__device__ __forceinline__ int chunk_slot(int x, int c) {
+  const int m = x & 15;
+  return c ^ (((m & 3) << 2) | (m >> 2));
 }
 
-// ---- the attention: one wave per 2 x 4 x 4 query block.
-__global__ __launch_bounds__(NWV * 64) __attribute__((amdgpu_waves_per_eu(2))) void na3d_fwd_kernel(NaArgs a) {
-  const int lane = threadIdx.x & 63, l32 = lane & 31, hi = lane >> 5;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+__global__ __launch_bounds__(NT) void na3d_fwd_kernel(NaArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t K0[BUF], K1[BUF], V0[BUF], V1[BUF];
+  const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   int lid;
   {  // workgroups go round-robin over the 8 XCDs: contiguous ranges per XCD
     const int i = blockIdx.x, n = a.nwg;
     const int per = n >> 3, rem = n & 7, xcd = i & 7, kk = i >> 3;
     lid = xcd < rem ? xcd * (per + 1) + kk : rem * (per + 1) + (xcd - rem) * per + kk;
   }
-  const int blk = lid * NWV + wave;
-  if (blk >= a.nblk) return;  // whole wave; there are no barriers
-  int x = blk;
+  int x = lid;
   const int bw = x % a.nbw;
   x /= a.nbw;
   const int bh = x % a.nbh;
@@ -147,27 +120,37 @@ __global__ __launch_bounds__(NWV * 64) __attribute__((amdgpu_waves_per_eu(2))) v
   const int bt = x % a.nbt;
   x /= a.nbt;
   const int h = x % a.H, b = x / a.H;
-  const int t0 = bt * QT, h0 = bh * QH, w0 = bw * QW;
+  const int t0 = bt * QT, h0 = bh * QH * WH, w0 = bw * QW * WW;
+  const int wi = wave / WW, wj = wave % WW;         // the wave's sub-block
+  const int sh0 = h0 + QH * wi, sw0 = w0 + QW * wj;
+  const bool wlive = sh0 < a.Hp && sw0 < a.Wp;       // uniform
 
   // the lane's query and its window
-  const int qt = t0 + (l32 >> 4), qh = h0 + ((l32 >> 2) & 3), qw = w0 + (l32 & 3);
+  const int qt = t0 + (l32 >> 4), qh = sh0 + ((l32 >> 2) & 3), qw = sw0 + (l32 & 3);
   const bool qlive = qt < a.T && qh < a.Hp && qw < a.Wp;
   const int2 wt = axis_window(min(qt, a.T - 1), a.T, a.kt, a.shift);
   const int2 wh = axis_window(min(qh, a.Hp - 1), a.Hp, a.kh, a.shift);
   const int2 ww = axis_window(min(qw, a.Wp - 1), a.Wp, a.kw, a.shift);
 
-  // the block's key box (windows are monotone in the query coordinate)
+  // the workgroup's key box (windows are monotone in the query coordinate):
+  // rows (t', h') and the staged w range [A0, A0 + 32)
   const int bt0 = axis_window(t0, a.T, a.kt, a.shift).x;
   const int bt1 = axis_window(min(t0 + QT - 1, a.T - 1), a.T, a.kt, a.shift).y;
   const int bh0 = axis_window(h0, a.Hp, a.kh, a.shift).x;
-  const int bh1 = axis_window(min(h0 + QH - 1, a.Hp - 1), a.Hp, a.kh, a.shift).y;
-  const int a0 = axis_window(w0, a.Wp, a.kw, a.shift).x & ~1;  // run start (even)
+  const int bh1 = axis_window(min(h0 + QH * WH - 1, a.Hp - 1), a.Hp, a.kh, a.shift).y;
+  const int A0 = axis_window(w0, a.Wp, a.kw, a.shift).x & ~1;
   const int nrh = bh1 - bh0 + 1;
-  const int nruns = (bt1 - bt0 + 1) * nrh;
-  const int nsb = (nruns + 1) >> 1;
+  const int nrows = (bt1 - bt0 + 1) * nrh;
+  const int nsteps = (nrows + 1) >> 1;
+  // the wave's rows h' and its 16-key run [a0, a0 + 16) of each staged row
+  const int wh0 = axis_window(min(sh0, a.Hp - 1), a.Hp, a.kh, a.shift).x;
+  const int wh1 = axis_window(min(sh0 + QH - 1, a.Hp - 1), a.Hp, a.kh, a.shift).y;
+  const int a0 = axis_window(min(sw0, a.Wp - 1), a.Wp, a.kw, a.shift).x & ~1;
+  const int off = a0 - A0;  // 0 .. 13
 
   // register i of a score accumulator holds key row 8 (i >> 2) + 4 hi + (i & 3)
-  // of the block: run i >> 3, position j(i) = 8 ((i >> 2) & 1) + 4 hi + (i & 3)
+  // of the block: row i >> 3 of the step, run position j(i) = 8 ((i >> 2) & 1)
+  // + 4 hi + (i & 3)
   bool wok[16];
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
@@ -176,16 +159,44 @@ __global__ __launch_bounds__(NWV * 64) __attribute__((amdgpu_waves_per_eu(2))) v
   }
 
   const int tok = a.H * D, rbytes = tok * 2;
-  const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(a.q + (size_t)b * a.L * tok), (short)0, a.L * rbytes, kBufferFlags);
   const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(a.k + (size_t)b * a.L * tok), (short)0, a.L * rbytes, kBufferFlags);
   const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(a.vt + ((size_t)b * a.H + h) * D * a.plane), (short)0, D * a.plane * 2, kBufferFlags);
+      (void*)(a.v + (size_t)b * a.L * tok), (short)0, a.L * rbytes, kBufferFlags);
+
+  // Rows (t', h') of the box are walked in order, two per step; a cursor
+  // holds the coordinates of the first row of a step.
+  auto advance = [&](int2 r, int n) __attribute__((always_inline)) {
+    r.y += n;
+    while (r.y > bh1) {
+      r.y -= nrh;
+      r.x += 1;
+    }
+    return r;
+  };
+  // staging: wave w copies 1 KB blocks 2 w, 2 w + 1 of each tensor, 4 keys a
+  // block (keys 0 .. 31 from the step's first row, 32 .. 63 from its second,
+  // at w positions A0 .. A0 + 31; a missing second row repeats the first);
+  // lane i fills slot i & 15 of key 4 blk + (i >> 4)
+  const int skey0 = 8 * wave + (lane >> 4);  // block 2 w; block 2 w + 1 is key + 4
+  auto stage = [&](int stp, int2 rowA, uint16_t* kb, uint16_t* vb) __attribute__((always_inline)) {
+    const int2 rw = skey0 >= 32 && 2 * stp + 1 < nrows ? advance(rowA, 1) : rowA;  // uniform per wave
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int kx = skey0 + 4 * u;
+      const uint32_t goff = (uint32_t)(((rw.x * a.Hp + rw.y) * a.Wp + A0 + (kx & 31)) * rbytes + h * D * 2 +
+                                       chunk_slot(kx, lane & 15) * 16);
+      const int blk = 2 * wave + u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_ptr)(kb + blk * 512), 16, goff, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_ptr)(vb + blk * 512), 16, goff, 0, 0, 0);
+    }
+  };
 
   // Q as the B operand: lane = query, d-chunk 2 st + hi of k-step st
   bf16x8 qop[8];
   {
+    const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(a.q + (size_t)b * a.L * tok), (short)0, a.L * rbytes, kBufferFlags);
     const uint32_t qoff = qlive ? (uint32_t)(((qt * a.Hp + qh) * a.Wp + qw) * rbytes + h * D * 2) : 0xfffff000u;
 #pragma unroll
     for (int st = 0; st < 8; ++st) {
@@ -201,47 +212,41 @@ __global__ __launch_bounds__(NWV * 64) __attribute__((amdgpu_waves_per_eu(2))) v
   float mref = -INFINITY, lsum = 0.f;
   const uint32_t ones = 0x3f803f80u;  // bf16 (1, 1)
 
-  // runs r0, r1 of score block p: (t', h') rows of the box
-  auto run_row = [&](int r) __attribute__((always_inline)) {
-    const int tk = bt0 + r / nrh, hk = bh0 + r % nrh;
-    return make_int2(tk, hk);
-  };
-  auto load_k = [&](int p, u32x4 kreg[8]) __attribute__((always_inline)) {
-    const int r = min(2 * p + (l32 >> 4), nruns - 1);
-    const int2 rk2 = run_row(r);
-    const uint32_t koff = (uint32_t)(((rk2.x * a.Hp + rk2.y) * a.Wp + a0 + (l32 & 15)) * rbytes + h * D * 2);
+  // per-lane LDS element offsets: score operand (key row l32 of the block,
+  // chunk 2 st + hi) and transposing V reads (as in the dense kernel's V
+  // order: key 8 r + 4 hi + ((l & 15) >> 2) of a 16-key step, channels
+  // 32 mb + 16 ((l >> 4) & 1) + 4 (l & 3) .. + 3); the second row's keys are
+  // 32 further (same slot map), an immediate offset
+  int koffs[8], voffs[4][2];
+  {
+    const int kx = 32 * (l32 >> 4) + off + (l32 & 15);
 #pragma unroll
-    for (int st = 0; st < 8; ++st) kreg[st] = __builtin_amdgcn_raw_buffer_load_b128(rk, koff + (2 * st + hi) * 16, 0, 0);
-  };
-
-  u32x4 kcur[8];
-  if (nsb > 0) load_k(0, kcur);
-  for (int p = 0; p < nsb; ++p) {
-    const int r0 = 2 * p, r1 = min(2 * p + 1, nruns - 1);
-    const bool real1 = 2 * p + 1 < nruns;
-    const int2 row0 = run_row(r0), row1 = run_row(r1);
-    // V^T operand of both runs: lane = channel 32 mb + l32, keys 4 hi .. +3 and 8 + 4 hi .. +3
-    u32x2 vlo[2][4], vhi[2][4];
+    for (int st = 0; st < 8; ++st) koffs[st] = kx * D + chunk_slot(kx, 2 * st + hi) * 8;
+    const int vd = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) {
-      const int2 rw = k2 ? row1 : row0;
-      const uint32_t base = (uint32_t)(((rw.x * a.Hp + rw.y) * a.Wps + a0 + 4 * hi) * 2);
+    for (int r = 0; r < 2; ++r) {
+      const int kk = off + 8 * r + 4 * hi + ((lane & 15) >> 2);
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb) {
-        const uint32_t off = base + (uint32_t)((32 * mb + l32) * a.plane) * 2u;
-        vlo[k2][mb] = __builtin_amdgcn_raw_buffer_load_b64(rv, off, 0, 0);
-        vhi[k2][mb] = __builtin_amdgcn_raw_buffer_load_b64(rv, off + 16, 0, 0);
+        const int d = 32 * mb + vd;
+        voffs[mb][r] = kk * D + chunk_slot(kk, d >> 3) * 8 + (d & 7);
       }
     }
-    // scores of this block
-    f32x16 s = f32x16{};
-#pragma unroll
-    for (int st = 0; st < 8; ++st) s = mfma32(__builtin_bit_cast(bf16x8, kcur[st]), qop[st], s);
-    if (p + 1 < nsb) load_k(p + 1, kcur);
+  }
 
-    // the lane's query sees run r (rows t', h') and, within it, positions wok
-    const bool ok0 = qlive && row0.x >= wt.x && row0.x <= wt.y && row0.y >= wh.x && row0.y <= wh.y;
-    const bool ok1 = qlive && real1 && row1.x >= wt.x && row1.x <= wt.y && row1.y >= wh.x && row1.y <= wh.y;
+  auto step = [&](int2 rowA, bool realB, const uint16_t* kb, const uint16_t* vb) __attribute__((always_inline)) {
+    const int2 rowB = realB ? advance(rowA, 1) : rowA;
+    const bool useA = wlive && rowA.y >= wh0 && rowA.y <= wh1;
+    const bool useB = wlive && realB && rowB.y >= wh0 && rowB.y <= wh1;
+    if (!(useA || useB)) return;  // uniform: nothing of this step is in the wave's windows
+    f32x16 sc = f32x16{};
+#pragma unroll
+    for (int st = 0; st < 8; ++st) {
+      const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kb + koffs[st]);
+      sc = mfma32(kop, qop[st], sc);
+    }
+    const bool ok0 = qlive && useA && rowA.x >= wt.x && rowA.x <= wt.y && rowA.y >= wh.x && rowA.y <= wh.y;
+    const bool ok1 = qlive && useB && rowB.x >= wt.x && rowB.x <= wt.y && rowB.y >= wh.x && rowB.y <= wh.y;
     bf16x8 pop[2];
     auto probs = [&]() __attribute__((always_inline)) {
       const float nm0 = ok0 ? -mref : -INFINITY, nm1 = ok1 ? -mref : -INFINITY;
@@ -252,8 +257,8 @@ __global__ __launch_bounds__(NWV * 64) __attribute__((amdgpu_waves_per_eu(2))) v
 #pragma unroll
         for (int e = 0; e < 8; e += 2) {
           const int i = 8 * k2 + e;
-          const float p0 = wok[i] ? __builtin_amdgcn_exp2f(fmaf(s[i], a.c, k2 ? nm1 : nm0)) : 0.f;
-          const float p1 = wok[i + 1] ? __builtin_amdgcn_exp2f(fmaf(s[i + 1], a.c, k2 ? nm1 : nm0)) : 0.f;
+          const float p0 = wok[i] ? __builtin_amdgcn_exp2f(fmaf(sc[i], a.c, k2 ? nm1 : nm0)) : 0.f;
+          const float p1 = wok[i + 1] ? __builtin_amdgcn_exp2f(fmaf(sc[i + 1], a.c, k2 ? nm1 : nm0)) : 0.f;
           pw[e >> 1] = pack_bf16x2(p0, p1);
           tsum = dot2(pw[e >> 1], ones, tsum);
         }
@@ -267,7 +272,7 @@ __global__ __launch_bounds__(NWV * 64) __attribute__((amdgpu_waves_per_eu(2))) v
       float m = -INFINITY;
 #pragma unroll
       for (int i = 0; i < 16; ++i)
-        if (wok[i] && (i < 8 ? ok0 : ok1)) m = fmaxf(m, s[i]);
+        if (wok[i] && (i < 8 ? ok0 : ok1)) m = fmaxf(m, sc[i]);
       const float m2 = wave_half_max(m);
       const float mnew = fmaxf(mref, m2 == -INFINITY ? -INFINITY : m2 * a.c);
       const float alpha = mnew == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(mref - mnew);
@@ -280,15 +285,37 @@ __global__ __launch_bounds__(NWV * 64) __attribute__((amdgpu_waves_per_eu(2))) v
       tsum = probs();
     }
     lsum += tsum;
-    // O^T += V^T P^T
+    // O^T += V^T P^T, one 16-key step per staged row
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb) {
-        const u32x4 w4 = {vlo[k2][mb][0], vlo[k2][mb][1], vhi[k2][mb][0], vhi[k2][mb][1]};
-        oacc[mb] = mfma32(__builtin_bit_cast(bf16x8, w4), pop[k2], oacc[mb]);
+        i16x4 part[2];
+#pragma unroll
+        for (int r = 0; r < 2; ++r) part[r] = lds_read_tr16(vb + voffs[mb][r] + 32 * k2 * D);
+        const bf16x8 vop = __builtin_bit_cast(bf16x8, __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7));
+        oacc[mb] = mfma32(vop, pop[k2], oacc[mb]);
       }
+  };
+
+  int2 cur = make_int2(bt0, bh0);  // first row of step s
+  stage(0, cur, K0, V0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  int s = 0;
+  for (; s + 1 < nsteps; s += 2) {
+    const int2 nxt = advance(cur, 2);
+    stage(s + 1, nxt, K1, V1);
+    step(cur, 2 * s + 1 < nrows, K0, V0);
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's copies have landed
+    __syncthreads();
+    cur = advance(nxt, 2);
+    if (s + 2 < nsteps) stage(s + 2, cur, K0, V0);
+    step(nxt, 2 * s + 3 < nrows, K1, V1);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
   }
+  if (s < nsteps) step(cur, 2 * s + 1 < nrows, K0, V0);
 
   // ---- output: O = O^T / l, lse = (m + log2 l) ln 2; lane holds its query,
   // d = 32 mb + 8 g + 4 hi + (0..3)
@@ -312,30 +339,20 @@ __global__ __launch_bounds__(NWV * 64) __attribute__((amdgpu_waves_per_eu(2))) v
 
 }  // namespace
 
-size_t na3d_workspace_elems(int B, int H, int T, int Hp, int Wp) {
-  const size_t wps = ((size_t)Wp + 7) / 8 * 8;
-  return (size_t)B * H * D * T * Hp * wps;
-}
-
-hipError_t launch_na3d_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o, float* lse,
-                           uint16_t* vt, int B, int H, int T, int Hp, int Wp, int kt, int kh, int kw, int shift,
-                           float scale, hipStream_t stream) {
+hipError_t launch_na3d_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o, float* lse, int B,
+                           int H, int T, int Hp, int Wp, int kt, int kh, int kw, int shift, float scale,
+                           hipStream_t stream) {
   NaArgs a;
-  a.q = q; a.k = k; a.vt = vt; a.o = o; a.lse = lse;
+  a.q = q; a.k = k; a.v = v; a.o = o; a.lse = lse;
   a.B = B; a.H = H; a.T = T; a.Hp = Hp; a.Wp = Wp; a.L = T * Hp * Wp;
-  a.Wps = (Wp + 7) / 8 * 8;
-  a.plane = T * Hp * a.Wps;
   a.kt = kt; a.kh = kh; a.kw = kw; a.shift = shift;
   a.c = fabsf(scale) * kLog2e;
   a.qsign = scale < 0.f ? 0x80008000u : 0u;
   a.nbt = (T + QT - 1) / QT;
-  a.nbh = (Hp + QH - 1) / QH;
-  a.nbw = (Wp + QW - 1) / QW;
-  a.nblk = B * H * a.nbt * a.nbh * a.nbw;
-  a.nwg = (a.nblk + NWV - 1) / NWV;
-  const int ntr = B * H * T * Hp * ((a.Wps + 63) / 64);
-  hipLaunchKernelGGL(na3d_transpose_v_kernel, dim3((unsigned)ntr), dim3(256), 0, stream, v, vt, a);
-  hipLaunchKernelGGL(na3d_fwd_kernel, dim3((unsigned)a.nwg), dim3(NWV * 64), 0, stream, a);
+  a.nbh = (Hp + QH * WH - 1) / (QH * WH);
+  a.nbw = (Wp + QW * WW - 1) / (QW * WW);
+  a.nwg = B * H * a.nbt * a.nbh * a.nbw;
+  hipLaunchKernelGGL(na3d_fwd_kernel, dim3((unsigned)a.nwg), dim3(NT), 0, stream, a);
   return hipGetLastError();
 }
 

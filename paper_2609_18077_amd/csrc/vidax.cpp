@@ -224,17 +224,9 @@ vidax_status vidax_attn_fwd_naive(const void* q, const void* k, const void* v, v
   return attn_common(AttnImpl::kNaive, q, k, v, o, lse, B, H, Lq, Lk, d, scale, kv_valid_len, rope, stream);
 }
 
-int64_t vidax_na3d_workspace_bytes(int32_t B, int32_t H, int32_t grid_t, int32_t grid_h, int32_t grid_w) {
-  if (B < 0 || H < 0 || grid_t < 0 || grid_h < 0 || grid_w < 0) return -1;
-  const int64_t wps = ((int64_t)grid_w + 7) / 8 * 8;
-  const int64_t n = numel4(B, H, (int64_t)vidax::kHeadDim * grid_t, (int64_t)grid_h * wps);
-  return n < 0 ? -1 : 2 * n;
-}
-
-vidax_status vidax_na3d_fwd(const void* q, const void* k, const void* v, void* o, float* lse, void* workspace,
-                            int64_t workspace_bytes, int32_t B, int32_t H, int32_t grid_t, int32_t grid_h,
-                            int32_t grid_w, int32_t d, int32_t win_t, int32_t win_h, int32_t win_w, int32_t border,
-                            float scale, hipStream_t stream) {
+vidax_status vidax_na3d_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int32_t B, int32_t H,
+                            int32_t grid_t, int32_t grid_h, int32_t grid_w, int32_t d, int32_t win_t, int32_t win_h,
+                            int32_t win_w, int32_t border, float scale, hipStream_t stream) {
   if (B < 0 || H < 0 || grid_t < 0 || grid_h < 0 || grid_w < 0 || d < 0) return VIDAX_ERR_INVALID_ARG;
   for (int32_t w : {win_t, win_h, win_w})
     if (w < 1 || (w & 1) == 0) return VIDAX_ERR_INVALID_ARG;
@@ -243,37 +235,26 @@ vidax_status vidax_na3d_fwd(const void* q, const void* k, const void* v, void* o
   const int64_t L = (int64_t)grid_t * grid_h * grid_w;
   const int64_t n = numel4(B, L, H, d);
   if (n < 0) return VIDAX_ERR_INVALID_ARG;
-  const int64_t need = vidax_na3d_workspace_bytes(B, H, grid_t, grid_h, grid_w);
-  if (need < 0) return VIDAX_ERR_INVALID_ARG;
-  if (n > 0 && (!q || !k || !v || !o || !workspace)) return VIDAX_ERR_INVALID_ARG;
-  for (const void* p : {q, k, v, (const void*)o, (const void*)workspace})
+  if (n > 0 && (!q || !k || !v || !o)) return VIDAX_ERR_INVALID_ARG;
+  for (const void* p : {q, k, v, (const void*)o})
     if (!aligned(p, 16)) return VIDAX_ERR_INVALID_ARG;
   if (!aligned(lse, 4)) return VIDAX_ERR_INVALID_ARG;
   if (d != vidax::kHeadDim) return VIDAX_ERR_UNSUPPORTED;
   if (win_w > 11) return VIDAX_ERR_UNSUPPORTED;  // a wave's key runs are 16 positions along w
   if (n == 0) return VIDAX_OK;
-  if (workspace_bytes < need) return VIDAX_ERR_INVALID_ARG;
   const uint64_t xb = (uint64_t)n * 2, lb = lse ? (uint64_t)B * H * L * 4 : 0;
-  // outputs (o, lse, the workspace) must not overlap each other or an input
-  const void* outs[3] = {o, lse, workspace};
-  const uint64_t osz[3] = {xb, lb, (uint64_t)need};
-  for (int i = 0; i < 3; ++i) {
-    for (const void* in : {q, k, v})
-      if (overlaps(outs[i], osz[i], in, xb)) return VIDAX_ERR_INVALID_ARG;
-    for (int j = i + 1; j < 3; ++j)
-      if (overlaps(outs[i], osz[i], outs[j], osz[j])) return VIDAX_ERR_INVALID_ARG;
-  }
-  // 32-bit buffer offsets: one batch of q/k (plus a run past its end) and one
-  // (b, h) plane of the workspace; launch sizes
-  const int64_t wps = ((int64_t)grid_w + 7) / 8 * 8;
-  if ((L + 16) * H * 256 > INT32_MAX || (int64_t)vidax::kHeadDim * grid_t * grid_h * wps * 2 > INT32_MAX)
-    return VIDAX_ERR_UNSUPPORTED;
-  const int64_t nblk = (int64_t)B * H * ((grid_t + 1) / 2) * ((grid_h + 3) / 4) * ((grid_w + 3) / 4);
-  const int64_t ntr = (int64_t)B * H * grid_t * grid_h * ((wps + 63) / 64);
-  if (nblk > INT32_MAX || ntr > INT32_MAX) return VIDAX_ERR_UNSUPPORTED;
-  const hipError_t e = vidax::launch_na3d_fwd((const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
-                                              (uint16_t*)o, lse, (uint16_t*)workspace, B, H, grid_t, grid_h, grid_w,
-                                              win_t, win_h, win_w, border, scale, stream);
+  // outputs must not overlap each other or an input
+  for (const void* in : {q, k, v})
+    if (overlaps(o, xb, in, xb) || overlaps(lse, lb, in, xb)) return VIDAX_ERR_INVALID_ARG;
+  if (overlaps(o, xb, lse, lb)) return VIDAX_ERR_INVALID_ARG;
+  // 32-bit buffer offsets within one batch (plus a staged row past its end);
+  // launch size
+  if ((L + 32) * H * 256 > INT32_MAX) return VIDAX_ERR_UNSUPPORTED;
+  const int64_t nwg = (int64_t)B * H * ((grid_t + 1) / 2) * ((grid_h + 7) / 8) * ((grid_w + 15) / 16);
+  if (nwg > INT32_MAX) return VIDAX_ERR_UNSUPPORTED;
+  const hipError_t e =
+      vidax::launch_na3d_fwd((const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, (uint16_t*)o, lse, B, H,
+                             grid_t, grid_h, grid_w, win_t, win_h, win_w, border, scale, stream);
   return e == hipSuccess ? VIDAX_OK : VIDAX_ERR_LAUNCH;
 }
 

@@ -159,34 +159,28 @@ def test_rope3d_transpose_rejects_invalid_arguments():
 
 def test_na3d_rejects_invalid_arguments():
     f = vx.lib().vidax_na3d_fwd
-    ws = vx.lib().vidax_na3d_workspace_bytes
     INV, UNS = 1, 2
-    need = ws(1, 2, 3, 5, 7)
-    assert need == 1 * 2 * 128 * 3 * 5 * 8 * 2
-    assert ws(-1, 2, 3, 5, 7) == -1
 
-    def call(q=P, k=2 * P, v=3 * P, o=4 * P, lse=5 * P, w=6 * P, wb=need, B=1, H=2, g=(3, 5, 7), d=128,
-             win=(3, 3, 3), border=0, scale=0.088):
+    def call(q=P, k=2 * P, v=3 * P, o=4 * P, lse=5 * P, B=1, H=2, g=(3, 5, 7), d=128, win=(3, 3, 3), border=0,
+             scale=0.088):
         ptr = lambda x: ctypes.c_void_p(x) if x else None
-        return f(ptr(q), ptr(k), ptr(v), ptr(o), ptr(lse), ptr(w), wb, B, H, *g, d, *win, border, scale, None)
+        return f(ptr(q), ptr(k), ptr(v), ptr(o), ptr(lse), B, H, *g, d, *win, border, scale, None)
 
     assert call(win=(2, 3, 3)) == INV       # even window
     assert call(win=(3, 0, 3)) == INV
     assert call(border=2) == INV
     assert call(scale=float("inf")) == INV
     assert call(q=0) == INV
-    assert call(w=0) == INV
-    assert call(wb=need - 2) == INV         # workspace too small
+    assert call(B=-1) == INV
     assert call(o=4 * P + 8) == INV         # misaligned
-    assert call(w=6 * P + 4) == INV
     assert call(lse=5 * P + 2) == INV
     assert call(d=64) == UNS
     assert call(win=(3, 3, 13)) == UNS      # w window beyond one 16-key run
     assert call(o=P) == INV                 # output aliases q
-    assert call(w=3 * P) == INV             # workspace aliases v
-    assert call(w=4 * P + 1024) == INV      # workspace overlaps o
-    assert call(B=0, q=0, k=0, v=0, o=0, lse=0, w=0, wb=0) == 0  # empty
-    assert call(g=(0, 5, 7), q=0, k=0, v=0, o=0, w=0, wb=0) == 0
+    assert call(lse=3 * P + 64) == INV      # lse inside v
+    assert call(lse=4 * P + 1024) == INV    # lse overlaps o
+    assert call(B=0, q=0, k=0, v=0, o=0, lse=0) == 0  # empty
+    assert call(g=(0, 5, 7), q=0, k=0, v=0, o=0) == 0
 
 
 def test_binding_fails_loudly_without_library(monkeypatch):
