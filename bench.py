@@ -252,6 +252,57 @@ def time_na3d(w, steps):
     return {name: {"ms": ms, "tflops": tf, "pct_bf16_peak": 100 * tf / PEAK_BF16_TFLOPS, "pairs": na3d_pairs(w)}}
 
 
+def time_cold(w, steps):
+    """The attention call with a 512 MB scratch write between calls, so that
+    Q, K, V do not start in the L2 / MALL (reported for the HBM-bound
+    cross-attention shape)."""
+    import torch
+
+    import paper_2609_18077_amd as vx
+    from paper_2609_18077_amd import inputs
+
+    q, k, v, lv = inputs.make_qkv(w)
+    up = lambda a: torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
+    qd, kd, vd = up(q), up(k), up(v)
+    ld = None if lv is None else torch.from_numpy(lv).cuda()
+    o = torch.empty_like(qd)
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    fn = lambda: vx.attn_fwd(qd, kd, vd, scale=w.scale, kv_valid_len=ld, out=o)
+    fn()
+    per = []
+    for _ in range(steps):
+        scratch.fill_(1)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn()
+        e1.record()
+        torch.cuda.synchronize()
+        per.append(e0.elapsed_time(e1))
+    ms = float(np.mean(per))
+    fl = flops(w, lv)
+    gbs = algorithmic_bytes(w, lv) / (ms * 1e-3) / 1e9
+    log(f"[bench] {w.name + ' (cold L2/MALL)':28s} {ms:9.3f} ms  {fl / ms / 1e9:8.1f} TFLOP/s  {gbs:8.1f} GB/s "
+        f"({100 * gbs / PEAK_HBM_GBS:.1f}% of HBM)")
+    return {w.name + "_cold": {"ms": ms, "tflops": fl / ms / 1e9, "algorithmic_GBs": gbs,
+                               "pct_hbm_peak": 100 * gbs / PEAK_HBM_GBS}}
+
+
+def environment():
+    """GPU, ROCm and host CPU for the record (the engine clock under load is
+    read from the SQ counters of the committed profiles, not here)."""
+    import torch
+
+    pr = torch.cuda.get_device_properties(0)
+    env = {"gpu": pr.name, "arch": getattr(pr, "gcnArchName", None), "cus": pr.multi_processor_count,
+           "hip": torch.version.hip, "torch": torch.__version__}
+    try:
+        with open("/proc/cpuinfo") as f:
+            env["host_cpu"] = next(l.split(":", 1)[1].strip() for l in f if l.startswith("model name"))
+    except (OSError, StopIteration):
+        env["host_cpu"] = None
+    return env
+
+
 def cpu_baseline(w, q, k, v, lv, budget_s=12.0):
     """The fp64 oracle on a bounded sample: whole heads of the same workload,
     all query rows, one head at a time until the time budget is used."""
@@ -375,6 +426,7 @@ def main():
             torch.cuda.empty_cache()
         for ww in inputs.NA_WORKLOADS.values():
             rows.update(time_na3d(ww, max(10, args.steps)))
+        rows.update(time_cold(inputs.WORKLOADS["cross_text"], max(10, args.steps // 2)))
         os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
         with open(os.path.join(ROOT, "gpurun_out", "bench_all.json"), "w") as f:
             json.dump(rows, f, indent=1)
@@ -420,9 +472,15 @@ def main():
             "traffic": traffic,
             "kernel": "attn_fwd_kernel",
             "kernel_ms_mean": round(r["event_ms_mean"], 4),
+            "kernel_ms_median": round(r["event_ms_median"], 4),
+            "kernel_ms_min": round(r["event_ms_min"], 4),
+            "kernel_ms_std": round(r["event_ms_std"], 4),
         },
         "alt": alt,
-        "cpu_baseline": None if cpu is None else {k2: cpu[k2] for k2 in ("value", "unit", "cores", "kind", "sample")},
+        "cpu_baseline": None if cpu is None else dict(
+            {k2: cpu[k2] for k2 in ("value", "unit", "cores", "kind", "sample")},
+            gpu_over_cpu=round(achieved / cpu["value"], 1)),
+        "env": environment(),
     }
     if extra:
         rec["all_workloads"] = extra["all_workloads"]
