@@ -26,7 +26,7 @@
 // than the 256 registers a wave has at two waves per SIMD.
 #include <type_traits>
 
-#include "common.hpp"
+#include "launch.hpp"
 
 namespace vidax {
 namespace {

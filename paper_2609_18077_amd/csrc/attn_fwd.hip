@@ -53,7 +53,7 @@
 // order (see below); rotary table <= 32 KB.
 #include <type_traits>
 
-#include "common.hpp"
+#include "launch.hpp"
 
 namespace vidax {
 namespace {

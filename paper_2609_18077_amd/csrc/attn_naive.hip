@@ -5,7 +5,7 @@
 // fp32 registers.  Keys and values are staged in LDS 32 at a time as fp32; the
 // rotation of each staged key is evaluated directly with sincosf (no table).
 // Softmax is the streaming form: running max, rescaled running sum.
-#include "common.hpp"
+#include "launch.hpp"
 
 namespace vidax {
 namespace {

@@ -87,26 +87,3 @@ __host__ __device__ inline PairSlot pair_slot(const RopeParams& r, int pi) {
 }
 
 }  // namespace vidax
-
-// Launchers implemented in the .hip files; called by the C ABI layer after
-// validation.  All pointers are device pointers; sizes already validated.
-namespace vidax {
-hipError_t launch_rope3d(const uint16_t* x, uint16_t* y, int B, int L, int H, const RopeParams& rp,
-                         hipStream_t stream);
-hipError_t launch_attn_bwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, const uint16_t* o,
-                           const uint16_t* dout, const float* lse, float* delta, uint16_t* dq, uint16_t* dk,
-                           uint16_t* dv, int B, int H, int Lq, int Lk, float scale, const int32_t* kv_valid_len,
-                           hipStream_t stream);
-hipError_t launch_qk_norm(const uint16_t* x, uint16_t* y, const float* gain, float eps, int B, int L, int H,
-                          const RopeParams& rp, hipStream_t stream);
-hipError_t launch_attn_naive(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o,
-                             float* lse, int B, int H, int Lq, int Lk, float scale,
-                             const int32_t* kv_valid_len, const RopeParams& rp, hipStream_t stream);
-bool attn_rope_supported(const RopeParams& rp);
-hipError_t launch_na3d_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o, float* lse, int B,
-                           int H, int T, int Hp, int Wp, int kt, int kh, int kw, int shift, float scale,
-                           hipStream_t stream);
-hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o,
-                           float* lse, int B, int H, int Lq, int Lk, float scale,
-                           const int32_t* kv_valid_len, const RopeParams& rp, hipStream_t stream);
-}  // namespace vidax

@@ -28,7 +28,7 @@
 // score reads), and any 4 consecutive keys put a 64-byte span in 4 different
 // quarters of the banks (the transposing reads).  Each 1 KB direct copy
 // fills 4 whole keys, 256 contiguous bytes of global memory each.
-#include "common.hpp"
+#include "launch.hpp"
 
 namespace vidax {
 namespace {

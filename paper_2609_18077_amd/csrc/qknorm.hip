@@ -10,7 +10,7 @@
 // (rotations within the 16-lane row, then permutations within quads), so
 // each lane ends with the row total without touching LDS.  Every lane reads
 // its chunk before any lane of the row writes, so y may alias x.
-#include "common.hpp"
+#include "launch.hpp"
 
 namespace vidax {
 namespace {

@@ -8,7 +8,7 @@
 // chunk, and applies them to the same chunk of every batch and head of that
 // token, so position decoding and table reads are amortised over B * H rows
 // and every global access is a 16-byte, row-contiguous load or store.
-#include "common.hpp"
+#include "launch.hpp"
 
 namespace vidax {
 namespace {

@@ -6,7 +6,7 @@
 #include <stdint.h>
 
 #include "../../include/vidax.h"
-#include "common.hpp"
+#include "launch.hpp"
 
 namespace {
 
