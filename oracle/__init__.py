@@ -18,7 +18,8 @@ method's arithmetic.
 served models (per-head RMS normalisation with a learned gain);
 ``attn_bwd_ref`` is the gradient of the attention (for post-training),
 ``rope_transpose_ref`` carries a gradient back through the rotation, and
-``na3d_ref`` is the 3D neighbourhood (windowed) attention of a VAE decoder.
+``na3d_ref`` is the 3D neighbourhood (windowed) attention of a VAE decoder,
+and ``qkv_proj_ref`` the Q/K/V projection followed by the Q/K prologue.
 """
 
 from .bf16 import bf16_bits_to_f64, f64_to_bf16_bits
@@ -27,6 +28,7 @@ from .attention import attn_ref, attn_ref_rows
 from .qknorm import qk_norm_ref
 from .attention_bwd import attn_bwd_ref, attn_bwd_ref_rows, rope_transpose_ref
 from .na3d import na3d_ref
+from .qkv import qkv_proj_ref
 
 __all__ = [
     "bf16_bits_to_f64",
@@ -41,4 +43,5 @@ __all__ = [
     "attn_bwd_ref_rows",
     "rope_transpose_ref",
     "na3d_ref",
+    "qkv_proj_ref",
 ]

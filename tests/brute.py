@@ -126,3 +126,33 @@ def na3d(q, k, v, scale, grid, window, border):
                     o[b][i][h][c] = math.fsum(ej * v[b][j][h][c] for ej, j in zip(e, keys)) / z
                 lse[b][h][i] = math.log(z)
     return o, lse
+
+
+def qkv_proj(x, w, bias, B, L, H, d, gain_q, gain_k, eps, rope):
+    """Projection, per-head RMS norm, gain and rotation with scalar loops.
+    x [M][C], w [3Hd][C], bias [3Hd] (lists); gains [d] lists or None;
+    rope = (grid, dims, theta, mode) or None.  Returns (q, k, v) as
+    nested lists [B][L][H][d]."""
+    C = len(x[0])
+    hd = H * d
+    out = []
+    for part in range(3):
+        t = [[[[0.0] * d for _ in range(H)] for _ in range(L)] for _ in range(B)]
+        gain = gain_q if part == 0 else gain_k if part == 1 else None
+        for b in range(B):
+            for n in range(L):
+                m = b * L + n
+                for h in range(H):
+                    row = []
+                    for c in range(d):
+                        col = part * hd + h * d + c
+                        acc = math.fsum(x[m][cc] * w[col][cc] for cc in range(C))
+                        row.append(acc + (bias[col] if bias is not None else 0.0))
+                    if part < 2:
+                        r = 1.0 / math.sqrt(math.fsum(z * z for z in row) / d + eps)
+                        row = [z * r * (gain[c] if gain is not None else 1.0) for c, z in enumerate(row)]
+                        if rope is not None:
+                            row = rope_row(row, n, *rope)
+                    t[b][n][h] = row
+        out.append(t)
+    return tuple(out)

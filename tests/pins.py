@@ -521,3 +521,72 @@ def check_na_interior_agree(na_fn, attn_fn):
 
 
 ALL_NA_CHECKS = [check_na_brute, check_na_full_window, check_na_single_key, check_na_interior_agree]
+
+
+# ------------------------------------------------------ Q/K/V projection ---
+
+def _qkv_case(rng, B=1, L=6, H=2, d=12, C=10):
+    x = rng.standard_normal((B * L, C))
+    w = rng.standard_normal((3 * H * d, C)) / np.sqrt(C)
+    bias = 0.3 * rng.standard_normal(3 * H * d)
+    gq = 1.0 + 0.2 * rng.standard_normal(d)
+    gk = 1.0 + 0.2 * rng.standard_normal(d)
+    return x, w, bias, gq, gk
+
+
+def check_qkv_brute(qkv_fn, spec_cls):
+    """Against scalar loops (projection, norm, gain, complex rotation)."""
+    from tests import brute
+
+    rng = _rng(71)
+    B, L, H, d = 2, 6, 2, 12
+    x, w, bias, gq, gk = _qkv_case(rng, B, L, H, d)
+    grid, dims = (1, 2, 3), (4, 4, 4)
+    spec = spec_cls(grid=grid, dims=dims, theta=50.0)
+    got = qkv_fn(x, w, bias, B, L, H, d, gq, gk, 1e-5, spec)
+    ref = brute.qkv_proj(x.tolist(), w.tolist(), bias.tolist(), B, L, H, d, gq.tolist(), gk.tolist(), 1e-5,
+                         (grid, dims, 50.0, 0))
+    for g, r in zip(got, ref):
+        assert np.allclose(g, np.array(r), rtol=1e-11, atol=1e-12)
+
+
+def check_qkv_permutation_weight(qkv_fn, spec_cls):
+    """A permutation weight picks input channels: output channel n of the
+    projection is x[:, pi(n)] (tests the orientation of W and the q, k, v
+    order of its rows)."""
+    rng = _rng(72)
+    B, L, H, d = 1, 5, 2, 8
+    C = 3 * H * d
+    x = rng.standard_normal((B * L, C))
+    pi = rng.permutation(C)
+    w = np.zeros((C, C))
+    w[np.arange(C), pi] = 1.0
+    q, k, v = qkv_fn(x, w, None, B, L, H, d, None, None, 0.0, None)
+    y = x[:, pi]
+    hd = H * d
+
+    def normed(z):
+        z = z.reshape(B, L, H, d)
+        return z / np.sqrt(np.mean(z * z, axis=-1, keepdims=True))
+
+    assert np.allclose(v, y[:, 2 * hd:].reshape(B, L, H, d), rtol=1e-14, atol=0)
+    assert np.allclose(q, normed(y[:, :hd]), rtol=1e-12, atol=1e-14)
+    assert np.allclose(k, normed(y[:, hd:2 * hd]), rtol=1e-12, atol=1e-14)
+
+
+def check_qkv_scale_and_gains(qkv_fn, spec_cls):
+    """Without bias, scaling x by a > 0 leaves q and k alone and scales v;
+    each gain acts on its own part only."""
+    rng = _rng(73)
+    B, L, H, d = 1, 4, 3, 8
+    x, w, _, gq, gk = _qkv_case(rng, B, L, H, d, C=9)
+    spec = spec_cls(grid=(1, 2, 2), dims=(2, 2, 4), theta=100.0)
+    q, k, v = qkv_fn(x, w, None, B, L, H, d, gq, gk, 1e-9, spec)
+    q2, k2, v2 = qkv_fn(3.5 * x, w, None, B, L, H, d, gq, gk, 1e-9, spec)
+    assert np.allclose(q2, q, rtol=1e-8) and np.allclose(k2, k, rtol=1e-8)
+    assert np.allclose(v2, 3.5 * v, rtol=1e-12)
+    q3, k3, v3 = qkv_fn(x, w, None, B, L, H, d, 2.0 * gq, gk, 1e-9, spec)
+    assert np.allclose(q3, 2.0 * q, rtol=1e-12) and np.allclose(k3, k, rtol=1e-14) and np.allclose(v3, v)
+
+
+ALL_QKV_CHECKS = [check_qkv_brute, check_qkv_permutation_weight, check_qkv_scale_and_gains]

@@ -371,3 +371,49 @@ def test_na_keys_mutation_is_caught(name, monkeypatch):
 
 def test_na_scale_dropped_is_caught():
     assert _na_caught(_na_scale_dropped)
+
+
+# ------------------------------------------------------ Q/K/V projection ---
+
+from oracle.qknorm import qk_norm_ref as _qkn  # noqa: E402
+
+
+def _qkv_mutant(kind):
+    def f(x, w, bias, B, L, H, d, gain_q=None, gain_k=None, eps=1e-6, rope=None, token_index=None):
+        x = np.asarray(x, dtype=np.float64)
+        w = np.asarray(w, dtype=np.float64)
+        y = x @ (w if kind == "weight_not_transposed" else w.T)
+        if bias is not None and kind != "bias_after_norm":
+            y = y + bias
+        hd = H * d
+        q = y[:, :hd].reshape(B, L, H, d)
+        k = y[:, hd:2 * hd].reshape(B, L, H, d)
+        v = y[:, 2 * hd:].reshape(B, L, H, d)
+        if kind == "q_k_blocks_swapped":
+            q, k = k, q
+        gq, gk = (gain_k, gain_q) if kind == "gains_swapped" else (gain_q, gain_k)
+        q = _qkn(q, gq, eps, rope, token_index=token_index)
+        k = _qkn(k, gk, eps, None if kind == "k_not_rotated" else rope, token_index=token_index)
+        if kind == "v_normalised":
+            v = _qkn(v, None, eps, None)
+        if kind == "bias_after_norm" and bias is not None:
+            q = q + np.asarray(bias[:hd]).reshape(H, d)
+            k = k + np.asarray(bias[hd:2 * hd]).reshape(H, d)
+            v = v + np.asarray(bias[2 * hd:]).reshape(H, d)
+        return q, k, v
+    return f
+
+
+QKV_MUTATIONS = ["weight_not_transposed", "bias_after_norm", "q_k_blocks_swapped", "gains_swapped", "v_normalised",
+                 "k_not_rotated"]
+
+
+@pytest.mark.parametrize("kind", QKV_MUTATIONS)
+def test_qkv_mutation_is_caught(kind):
+    fn = _qkv_mutant(kind)
+    for check in pins.ALL_QKV_CHECKS:
+        try:
+            check(fn, RopeSpec)
+        except (AssertionError, ValueError):  # a shape error is a caught mistake too
+            return
+    raise AssertionError(kind + " went unnoticed")

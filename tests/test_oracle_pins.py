@@ -93,3 +93,8 @@ def test_bwd_rows_subset():
 @pytest.mark.parametrize("check", pins.ALL_NA_CHECKS, ids=lambda c: c.__name__)
 def test_na_pins(check):
     check(oracle.na3d_ref, oracle.attn_ref)
+
+
+@pytest.mark.parametrize("check", pins.ALL_QKV_CHECKS, ids=lambda c: c.__name__)
+def test_qkv_pins(check):
+    check(oracle.qkv_proj_ref, oracle.RopeSpec)
