@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define VIDAX_ABI_VERSION 5
+#define VIDAX_ABI_VERSION 6
 
 typedef enum vidax_status {
   VIDAX_OK = 0,
@@ -205,6 +205,28 @@ vidax_status vidax_attn_bwd(const void* q, const void* k, const void* v, const v
 vidax_status vidax_na3d_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int32_t B, int32_t H,
                             int32_t grid_t, int32_t grid_h, int32_t grid_w, int32_t d, int32_t win_t, int32_t win_h,
                             int32_t win_w, int32_t border, float scale, hipStream_t stream);
+
+/*
+ * Q/K/V projection with the query/key prologue in its epilogue: the step that
+ * produces an attention call's inputs in the served video DiTs (Section 3,
+ * "Supported Models"; rotation as in Section 2).  With M = B * L tokens,
+ *
+ *   y = x W^T (+ bias)           x: bf16 [M, C], W: bf16 [3 H d, C] (rows =
+ *                                output channels: q heads, k heads, v heads),
+ *                                bias: fp32 [3 H d] or NULL
+ *   q = rope(rms_norm(y_q) * gain_q),  k = rope(rms_norm(y_k) * gain_k),  v = y_v
+ *
+ * where rms_norm acts on each (token, head) over its d channels with eps, as
+ * in vidax_qk_norm_rope; gains fp32 [d] (shared by the heads) or NULL (unit);
+ * rope as vidax_rope3d (token n of each sequence of L, interleaved pairs
+ * only), or NULL for none.  q, k, v: bf16 [B, L, H, d] outputs, rounded once.
+ * fp32 accumulation.  All pointers 16-byte aligned; outputs must not overlap
+ * each other or an input.  Requires d == 128 and C a multiple of 64
+ * (VIDAX_ERR_UNSUPPORTED otherwise); eps >= 0 finite.
+ */
+vidax_status vidax_qkv_proj(const void* x, const void* w, const float* bias, const float* gain_q,
+                            const float* gain_k, float eps, void* q, void* k, void* v, int32_t B, int32_t L,
+                            int32_t H, int32_t d, int32_t C, const vidax_rope3d_desc* rope, hipStream_t stream);
 
 /*
  * Same contract as vidax_attn_fwd, computed by a plain scalar fp32 kernel (one

@@ -24,6 +24,7 @@ EXPORTED_SYMBOLS = (
     "vidax_rope3d_transpose",
     "vidax_attn_bwd",
     "vidax_na3d_fwd",
+    "vidax_qkv_proj",
     "vidax_qk_norm_rope",
     "vidax_attn_fwd",
     "vidax_attn_fwd_naive",
@@ -90,6 +91,8 @@ def lib() -> ctypes.CDLL:
         L.vidax_attn_bwd.restype = i32
         L.vidax_na3d_fwd.argtypes = [vp] * 5 + [i32] * 10 + [f32, vp]
         L.vidax_na3d_fwd.restype = i32
+        L.vidax_qkv_proj.argtypes = [vp] * 5 + [f32] + [vp] * 3 + [i32] * 5 + [ctypes.POINTER(RopeDesc), vp]
+        L.vidax_qkv_proj.restype = i32
         L.vidax_qk_norm_rope.argtypes = [vp, vp, vp, f32, i32, i32, i32, i32, ctypes.POINTER(RopeDesc), vp]
         L.vidax_qk_norm_rope.restype = i32
         for name in ("vidax_attn_fwd", "vidax_attn_fwd_naive"):
@@ -209,6 +212,33 @@ def na3d_fwd(q, k, v, grid, window=(11, 11, 11), border: str = "clip", scale=Non
                                                   *(int(x) for x in window), 0 if border == "clip" else 1,
                                                   float(scale), _stream(stream)))
     return (o, lse) if return_lse else o
+
+
+def qkv_proj(x, w, B: int, L: int, H: int, bias=None, gain_q=None, gain_k=None, eps: float = 1e-6,
+             rope: Rope | None = None, stream=None):
+    """(q, k, v) bf16 [B, L, H, 128] from hidden states x (bf16 [B*L, C]) and
+    the projection weight w (bf16 [3*H*128, C]); q and k RMS-normalised per
+    head, gained and rotated."""
+    import torch
+
+    for n, t in (("x", x), ("w", w)):
+        if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous() or t.dim() != 2:
+            raise ValueError(f"{n} must be a contiguous 2-D bfloat16 device tensor")
+    C = x.shape[1]
+    d = w.shape[0] // (3 * H) if H > 0 else 0
+    if x.shape[0] != B * L or w.shape[1] != C or w.shape[0] != 3 * H * d:
+        raise ValueError("x must be [B*L, C] and w [3*H*d, C]")
+    for n, t, size in (("bias", bias, 3 * H * d), ("gain_q", gain_q, d), ("gain_k", gain_k, d)):
+        if t is not None and (t.dtype != torch.float32 or not t.is_cuda or not t.is_contiguous()
+                              or t.numel() != size):
+            raise ValueError(f"{n} must be a contiguous float32 device tensor of {size} elements")
+    q, k, v = (torch.empty((B, L, H, d), dtype=torch.bfloat16, device=x.device) for _ in range(3))
+    desc = rope.desc() if rope is not None else None
+    _check("vidax_qkv_proj", lib().vidax_qkv_proj(_ptr(x), _ptr(w), _ptr(bias), _ptr(gain_q), _ptr(gain_k),
+                                                  float(eps), _ptr(q), _ptr(k), _ptr(v), B, L, H, d, C,
+                                                  ctypes.byref(desc) if desc is not None else None,
+                                                  _stream(stream)))
+    return q, k, v
 
 
 def qk_norm_rope(x, rope: Rope | None = None, gain=None, eps: float = 1e-6, out=None, stream=None):

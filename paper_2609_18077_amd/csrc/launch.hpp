@@ -26,4 +26,7 @@ hipError_t launch_na3d_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
 hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o,
                            float* lse, int B, int H, int Lq, int Lk, float scale,
                            const int32_t* kv_valid_len, const RopeParams& rp, hipStream_t stream);
+hipError_t launch_qkv_proj(const uint16_t* x, const uint16_t* w, const float* bias, const float* gain_q,
+                           const float* gain_k, float eps, uint16_t* q, uint16_t* k, uint16_t* v, int B, int L, int H,
+                           int C, const RopeParams& rp, hipStream_t stream);
 }  // namespace vidax

@@ -258,6 +258,49 @@ vidax_status vidax_na3d_fwd(const void* q, const void* k, const void* v, void* o
   return e == hipSuccess ? VIDAX_OK : VIDAX_ERR_LAUNCH;
 }
 
+vidax_status vidax_qkv_proj(const void* x, const void* w, const float* bias, const float* gain_q,
+                            const float* gain_k, float eps, void* q, void* k, void* v, int32_t B, int32_t L,
+                            int32_t H, int32_t d, int32_t C, const vidax_rope3d_desc* rope, hipStream_t stream) {
+  if (B < 0 || L < 0 || H < 0 || d < 0 || C < 0) return VIDAX_ERR_INVALID_ARG;
+  const int64_t M = (int64_t)B * L;
+  const int64_t nx = numel4(M, C, 1, 1), nw = numel4(3, H, d, C), no = numel4(M, H, d, 1);
+  if (nx < 0 || nw < 0 || no < 0) return VIDAX_ERR_INVALID_ARG;
+  if (!(eps >= 0.0f) || !isfinite(eps)) return VIDAX_ERR_INVALID_ARG;
+  if (no > 0 && (!q || !k || !v || (C > 0 && (!x || !w)))) return VIDAX_ERR_INVALID_ARG;
+  for (const void* p : {x, w, (const void*)bias, (const void*)gain_q, (const void*)gain_k, (const void*)q,
+                        (const void*)k, (const void*)v})
+    if (!aligned(p, 16)) return VIDAX_ERR_INVALID_ARG;
+  if (d != vidax::kHeadDim) return VIDAX_ERR_UNSUPPORTED;
+  if (C % 64 != 0 || (C == 0 && no > 0)) return VIDAX_ERR_UNSUPPORTED;  // stages of 64 input channels
+  RopeParams rp = no_rope();
+  if (rope) {
+    vidax_rope3d_desc r = *rope;
+    r.keys_prerotated = 0;  // attention-only field
+    const vidax_status st = make_rope(&r, L, d, &rp);
+    if (st != VIDAX_OK) return st;
+    if (rp.pair_mode != 0) return VIDAX_ERR_UNSUPPORTED;
+  }
+  if (no == 0) return VIDAX_OK;
+  const uint64_t ob = (uint64_t)no * 2;
+  const void* outs[3] = {q, k, v};
+  const void* ins[5] = {x, w, bias, gain_q, gain_k};
+  const uint64_t isz[5] = {(uint64_t)nx * 2, (uint64_t)nw * 2, bias ? (uint64_t)3 * H * d * 4 : 0,
+                           gain_q ? (uint64_t)d * 4 : 0, gain_k ? (uint64_t)d * 4 : 0};
+  for (int i = 0; i < 3; ++i) {
+    for (int j = 0; j < 5; ++j)
+      if (overlaps(outs[i], ob, ins[j], isz[j])) return VIDAX_ERR_INVALID_ARG;
+    for (int j = i + 1; j < 3; ++j)
+      if (overlaps(outs[i], ob, outs[j], ob)) return VIDAX_ERR_INVALID_ARG;
+  }
+  // 32-bit buffer offsets within a 256-row tile; launch size
+  if ((int64_t)256 * C * 2 > INT32_MAX) return VIDAX_ERR_UNSUPPORTED;
+  const int64_t nwg = ((int64_t)3 * H * d + 255) / 256 * ((M + 255) / 256);
+  if (nwg > INT32_MAX || M > INT32_MAX) return VIDAX_ERR_UNSUPPORTED;
+  const hipError_t e = vidax::launch_qkv_proj((const uint16_t*)x, (const uint16_t*)w, bias, gain_q, gain_k, eps,
+                                              (uint16_t*)q, (uint16_t*)k, (uint16_t*)v, B, L, H, C, rp, stream);
+  return e == hipSuccess ? VIDAX_OK : VIDAX_ERR_LAUNCH;
+}
+
 const char* vidax_status_string(vidax_status s) {
   switch (s) {
     case VIDAX_OK: return "ok";

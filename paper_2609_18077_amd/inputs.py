@@ -36,6 +36,8 @@ HEAD_DIM = 128
 
 # tensor ids used in the seed sequence
 T_Q, T_K, T_V, T_LEN, T_DO = 0, 1, 2, 3, 4
+# projection inputs: hidden states, weight, bias, gains
+T_X, T_W, T_BIAS, T_GQ, T_GK = 5, 6, 7, 8, 9
 
 
 @dataclass(frozen=True)
@@ -147,10 +149,12 @@ def _rms_norm_rows(x: np.ndarray, d: int) -> np.ndarray:
     return x
 
 
-def bf16_tensor(seed: int, tensor_id: int, shape, rms_norm: bool = False) -> np.ndarray:
-    """A bfloat16 tensor (uint16 bits) of the given shape, drawn N(0,1)."""
+def bf16_tensor(seed: int, tensor_id: int, shape, rms_norm: bool = False, std: float = 1.0) -> np.ndarray:
+    """A bfloat16 tensor (uint16 bits) of the given shape, drawn N(0, std^2)."""
     n = int(np.prod(shape))
     x = normal_f32(seed, tensor_id, n)
+    if std != 1.0:
+        x *= np.float32(std)
     if rms_norm:
         x = _rms_norm_rows(x, shape[-1])
     out = np.empty(n, np.uint16)
@@ -230,6 +234,50 @@ def make_na_qkv(w: NaWorkload):
     """(q, k, v) uint16 bf16 bits [B, L, H, d] of a neighbourhood-attention workload."""
     shape = (w.B, w.L, w.H, w.d)
     return tuple(bf16_tensor(w.seed, t, shape) for t in (T_Q, T_K, T_V))
+
+
+@dataclass(frozen=True)
+class ProjWorkload:
+    """A Q/K/V projection of hidden states [B*L, C] into H heads of d, with the
+    rotary grid of the tokens (None: no rotation)."""
+
+    name: str
+    B: int
+    L: int
+    H: int
+    C: int
+    seed: int
+    grid: tuple | None = None
+    dims: tuple = (44, 42, 42)
+    theta: float = 10000.0
+    bias: bool = True
+    gains: bool = True
+    eps: float = 1e-6
+    d: int = HEAD_DIM
+    description: str = field(default="", compare=False)
+
+
+# Wan2.1-1.3B at 832 x 480, 81 frames: hidden size 1536 = 12 heads of 128
+PROJ_WORKLOADS = {
+    w.name: w
+    for w in [
+        ProjWorkload("wan13b_480p_qkv", B=1, L=32760, H=12, C=1536, seed=7, grid=(21, 30, 52),
+                     description="Wan2.1-1.3B 832x480 81f: QKV projection of 32760 tokens, hidden 1536"),
+    ]
+}
+
+
+def make_proj_inputs(w: ProjWorkload):
+    """(x bf16 [B*L, C], W bf16 [3 H d, C], bias fp32 [3 H d] or None, gain_q,
+    gain_k fp32 [d] or None): x ~ N(0, 1), W ~ N(0, 1/C) (unit-variance
+    outputs), bias ~ N(0, 0.1^2), gains ~ 1 + N(0, 0.1^2)."""
+    n = 3 * w.H * w.d
+    x = bf16_tensor(w.seed, T_X, (w.B * w.L, w.C))
+    wt = bf16_tensor(w.seed, T_W, (n, w.C), std=float(1.0 / np.sqrt(w.C)))
+    bias = 0.1 * normal_f32(w.seed, T_BIAS, n) if w.bias else None
+    gq = 1.0 + 0.1 * normal_f32(w.seed, T_GQ, w.d) if w.gains else None
+    gk = 1.0 + 0.1 * normal_f32(w.seed, T_GK, w.d) if w.gains else None
+    return x, wt, bias, gq, gk
 
 
 def custom(name="custom", **kw) -> Workload:

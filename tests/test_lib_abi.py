@@ -25,7 +25,7 @@ def test_library_exports_every_declared_function():
     assert set(declared) == set(vx.EXPORTED_SYMBOLS), declared
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.vidax_abi_version() == 5
+    assert lib.vidax_abi_version() == 6
     for s, text in [(0, b"ok"), (1, b"invalid argument"), (2, b"unsupported configuration"), (3, b"kernel launch failed")]:
         assert lib.vidax_status_string(s) == text
     assert lib.vidax_status_string(99) == b"unknown status"
@@ -181,6 +181,36 @@ def test_na3d_rejects_invalid_arguments():
     assert call(lse=4 * P + 1024) == INV    # lse overlaps o
     assert call(B=0, q=0, k=0, v=0, o=0, lse=0) == 0  # empty
     assert call(g=(0, 5, 7), q=0, k=0, v=0, o=0) == 0
+
+
+def test_qkv_proj_rejects_invalid_arguments():
+    f = vx.lib().vidax_qkv_proj
+    INV, UNS = 1, 2
+    good = vx.Rope((2, 4, 8), (44, 42, 42)).desc()
+
+    def call(x=P, w=2 * P, bias=3 * P, gq=4 * P, gk=5 * P, eps=1e-6, q=6 * P, k=7 * P, v=8 * P, B=1, L=64, H=2,
+             d=128, C=256, rope=None):
+        ptr = lambda a: ctypes.c_void_p(a) if a else None
+        return f(ptr(x), ptr(w), ptr(bias), ptr(gq), ptr(gk), eps, ptr(q), ptr(k), ptr(v), B, L, H, d, C,
+                 ctypes.byref(rope) if rope is not None else None, None)
+
+    assert call(x=0) == INV
+    assert call(q=0) == INV
+    assert call(B=-1) == INV
+    assert call(eps=-1.0) == INV
+    assert call(eps=float("nan")) == INV
+    assert call(bias=3 * P + 4) == INV      # misaligned
+    assert call(k=7 * P + 8) == INV
+    assert call(d=64) == UNS
+    assert call(C=96) == UNS                # not a multiple of 64
+    assert call(q=P) == INV                 # output aliases x
+    assert call(v=2 * P + 512) == INV       # output inside w
+    assert call(k=6 * P + 1024) == INV      # outputs overlap
+    bad = vx.Rope((2, 4, 8), (44, 42, 42), pair_mode=1).desc()
+    assert call(rope=bad) == UNS            # half-split pairs
+    assert call(rope=good, L=63) == INV     # more rotated tokens than L
+    assert call(B=0, x=0, w=0, q=0, k=0, v=0) == 0  # empty
+    assert call(bias=0, gq=0, gk=0, C=0, L=0) == 0
 
 
 def test_binding_fails_loudly_without_library(monkeypatch):
