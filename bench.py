@@ -252,6 +252,41 @@ def time_na3d(w, steps):
     return {name: {"ms": ms, "tflops": tf, "pct_bf16_peak": 100 * tf / PEAK_BF16_TFLOPS, "pairs": na3d_pairs(w)}}
 
 
+def time_qkv_proj(w, steps):
+    """vidax_qkv_proj (projection + Q/K prologue epilogue); FLOPs of the
+    product 2 M C N (the epilogue's norm and rotation are not counted)."""
+    import torch
+
+    import paper_2609_18077_amd as vx
+    from paper_2609_18077_amd import inputs
+
+    x, wt, bias, gq, gk = inputs.make_proj_inputs(w)
+    bf = lambda a: torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
+    f32 = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda()
+    xd, wd, bd, gqd, gkd = bf(x), bf(wt), f32(bias), f32(gq), f32(gk)
+    rope = vx.Rope(w.grid, w.dims, w.theta) if w.grid is not None else None
+    fn = lambda: vx.qkv_proj(xd, wd, w.B, w.L, w.H, bias=bd, gain_q=gqd, gain_k=gkd, eps=w.eps, rope=rope)
+    for _ in range(3):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    M, N = w.B * w.L, 3 * w.H * w.d
+    fl = 2.0 * M * w.C * N
+    byt = 2.0 * (M * w.C + N * w.C + 3 * M * w.H * w.d)
+    tf = fl / (ms * 1e-3) / 1e12
+    name = "qkv_proj_" + w.name
+    log(f"[bench] {name:28s} {ms:9.3f} ms  {tf:8.1f} TFLOP/s  {100 * tf / PEAK_BF16_TFLOPS:5.1f}%  "
+        f"{byt / (ms * 1e-3) / 1e9:8.1f} GB/s")
+    return {name: {"ms": ms, "tflops": tf, "pct_bf16_peak": 100 * tf / PEAK_BF16_TFLOPS,
+                   "algorithmic_GBs": byt / (ms * 1e-3) / 1e9}}
+
+
 def time_cold(w, steps):
     """The attention call with a 512 MB scratch write between calls, so that
     Q, K, V do not start in the L2 / MALL (reported for the HBM-bound
@@ -350,6 +385,8 @@ def main():
                     help="only time vidax_attn_bwd on the workload (stderr) and exit (for profiling the backward)")
     ap.add_argument("--na", action="store_true",
                     help="only time vidax_na3d_fwd on the neighbourhood-attention workloads (stderr) and exit")
+    ap.add_argument("--qkv", action="store_true",
+                    help="only time vidax_qkv_proj on the projection workloads (stderr) and exit")
     ap.add_argument("--calib-copy", type=int, default=0, metavar="MIB",
                     help="only run one plain device copy of MIB MiB (rocprofv3 counter calibration) and exit")
     args = ap.parse_args()
@@ -383,6 +420,10 @@ def main():
     if args.na:
         for ww in inputs.NA_WORKLOADS.values():
             time_na3d(ww, args.steps)
+        return
+    if args.qkv:
+        for ww in inputs.PROJ_WORKLOADS.values():
+            time_qkv_proj(ww, args.steps)
         return
     r = time_gpu(w, args.steps, args.warmup)
     q, k, v, lv = r.pop("inputs")
@@ -427,6 +468,8 @@ def main():
         for ww in inputs.NA_WORKLOADS.values():
             rows.update(time_na3d(ww, max(10, args.steps)))
         rows.update(time_cold(inputs.WORKLOADS["cross_text"], max(10, args.steps // 2)))
+        for ww in inputs.PROJ_WORKLOADS.values():
+            rows.update(time_qkv_proj(ww, max(10, args.steps)))
         os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
         with open(os.path.join(ROOT, "gpurun_out", "bench_all.json"), "w") as f:
             json.dump(rows, f, indent=1)

@@ -76,8 +76,13 @@ __global__ __launch_bounds__(NT) void qkv_proj_kernel(QkvArgs a) {
     const int per = n >> 3, rem = n & 7, xcd = i & 7, kk = i >> 3;
     lid = xcd < rem ? xcd * (per + 1) + kk : rem * (per + 1) + (xcd - rem) * per + kk;
   }
-  // channel tiles fastest: the workgroups that run together share their x rows
-  const int tn = lid % a.ntn, tm = lid / a.ntn;
+  // Groups of GM token tiles, token tiles fastest inside a group: the 32
+  // workgroups an XCD runs at a time then cover 8 token tiles x 4 channel
+  // tiles, whose weight rows (4 x 768 KB at C = 1536) stay in that XCD's L2.
+  constexpr int GM = 8;
+  const int g = lid / (GM * a.ntn), r = lid - g * GM * a.ntn;
+  const int gm = min(GM, a.ntm - g * GM);
+  const int tn = r / gm, tm = g * GM + (r - (r / gm) * gm);
   const int n0 = tn * BNC, m0 = tm * BMT;
   const int wh = wave & 1, wt = wave >> 1;  // the wave's head (of two) and token group
 
