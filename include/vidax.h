@@ -145,6 +145,9 @@ vidax_status vidax_qk_norm_rope(const void* x, void* y, const float* gain, float
  *   All Lq rows are computed; there is no causal mask.  Matrix products run
  *   on bf16 inputs with fp32 accumulation; the softmax is fp32.
  *   Requires d == 128; o must not alias q, k or v.  B, H, Lq, Lk >= 0.
+ *   One batch of a tensor, max(Lq, Lk) * H * d * 2 bytes, must stay below
+ *   2 GiB - 4 KiB (the kernels use 32-bit buffer offsets within a batch):
+ *   VIDAX_ERR_UNSUPPORTED beyond; vidax_attn_fwd_naive has the same limit.
  */
 vidax_status vidax_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
                             int32_t B, int32_t H, int32_t Lq, int32_t Lk, int32_t d, float scale,

@@ -99,6 +99,9 @@ vidax_status attn_common(AttnImpl impl, const void* q, const void* k, const void
     if (st != VIDAX_OK) return st;
     if (impl == AttnImpl::kMatrixCore && !vidax::attn_rope_supported(rp)) return VIDAX_ERR_UNSUPPORTED;
   }
+  // the kernels address one batch of q, o (and of k, v within a tile) with
+  // 32-bit buffer offsets: one batch of a tensor must stay below 2 GiB
+  if ((int64_t)(Lq > Lk ? Lq : Lk) * H * d * 2 > INT32_MAX - 4096) return VIDAX_ERR_UNSUPPORTED;
   // one workgroup per 256 (matrix core) or 64 (naive) query rows of each (b, h)
   const int64_t rows = impl == AttnImpl::kMatrixCore ? 256 : 64;
   const int64_t grid = ((int64_t)Lq + rows - 1) / rows * B * H;

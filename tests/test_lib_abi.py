@@ -56,6 +56,7 @@ def test_attn_rejects_invalid_arguments(fn):
     assert _attn(fn, scale=float("nan")) == INV
     assert _attn(fn, scale=float("inf")) == INV
     assert _attn(fn, d=64) == UNS
+    assert _attn(fn, H=64, Lq=140000, Lk=64) == UNS   # one batch of q beyond 2 GiB
     assert _attn(fn, o=P) == INV                # output aliases q
     assert _attn(fn, o=2 * P + 4096) == INV     # output overlaps k
     good = vx.Rope((1, 8, 8), (44, 42, 42)).desc()
