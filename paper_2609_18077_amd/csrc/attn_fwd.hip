@@ -49,8 +49,13 @@
 // key, so rows past kv_valid_len read as zero (and land in LDS as zero)
 // without any per-lane test.
 //
+// Query rows are loaded and output rows stored whole (coalesced), through a
+// per-wave staging area in LDS that converts to and from the layout in which
+// a lane holds one query.
+//
 // LDS (per workgroup): K and V tiles 2 x 16 KB each, stored in MFMA operand
-// order (see below); rotary table <= 32 KB.
+// order (see below); rotary table <= 32 KB; the persistent form adds a 64 KB
+// query/output staging buffer (the plain form stages in the K/V buffers).
 #include <type_traits>
 
 #include "launch.hpp"
@@ -164,6 +169,14 @@ __device__ __forceinline__ float2 table_entry(const float2* tab, const PairIdx& 
   return *reinterpret_cast<const float2*>(reinterpret_cast<const char*>(tab) + off);
 }
 
+// Slot of 16-byte chunk c of staging row r (an involution in c).  For any 16
+// consecutive rows and one chunk, and for any 4 rows x 4 chunks aligned by 4,
+// the slots are distinct, so the staging accesses are free of bank conflicts.
+__device__ __forceinline__ int stage_slot(int c, int r) {
+  const int x = r & 15;
+  return c ^ (((x & 3) << 2) | (x >> 2));
+}
+
 __device__ __forceinline__ uint32_t packed_pos(const AttnArgs& a, int n) {
   if (n >= a.rp.n_rot) return a.pos_sent;
   const int t = n / (a.rp.gh * a.rp.gw);
@@ -185,9 +198,11 @@ __device__ __forceinline__ uint32_t packed_pos(const AttnArgs& a, int n) {
 // block is filled by one direct 1 KB global -> LDS copy.
 constexpr int TILE = BN * D;  // elements per K or V tile
 constexpr int BLK = 512;      // elements per operand block
-constexpr int kOutStores = 17;  // store instructions per wave for one tile's output (O and LSE)
-// s_waitcnt immediate: vmcnt <= kOutStores, expcnt and lgkmcnt not waited for
-constexpr int kWaitCopiesBehindStores = (kOutStores & 15) | (7 << 4) | (15 << 8) | ((kOutStores >> 4) << 14);
+constexpr int kOutStores = 9;  // store instructions per wave for one tile's output (O and LSE)
+// s_waitcnt immediate: at most n vector memory operations outstanding (expcnt
+// and lgkmcnt not waited for)
+constexpr int wait_vm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
+constexpr int kQueryCopies = 8;  // staging copies per wave for one tile's queries
 #ifndef VIDAX_SHORT_KEYS
 #define VIDAX_SHORT_KEYS 2048
 #endif
@@ -210,6 +225,9 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   // (and does not wait for the copies before those reads).
   __shared__ __attribute__((aligned(16))) uint16_t K0[TILE], K1[TILE], V0[TILE], V1[TILE];
   __shared__ float2 tab[ROPE ? kAttnTableMax : 1];
+  // The persistent form copies the next tile's K/V while it stores the
+  // finished tile's output, so its query/output staging has its own buffer.
+  __shared__ __attribute__((aligned(16))) uint16_t QO[PERSIST ? NW * 32 * D : 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -253,15 +271,38 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
     ntiles = (lv + BN - 1) / BN;
   };
 
-  // raw query chunks 2s + hi (s = 0..7) of this lane's row of tile lid
-  auto load_q = [&](int lid, uint4 raw[8]) __attribute__((always_inline)) {
+  // Query rows come in and output rows go out whole: each 16-lane group of a
+  // wave moves one 256-byte row (coalesced), and the wave's 8 KB staging area
+  // in LDS (32 rows x 16 chunks of 16 bytes, chunk c of row r at slot
+  // stage_slot(c, r)) converts between that layout and the operand layout in
+  // which a lane holds one query.  The plain form borrows the K/V buffers
+  // (free before the first copies and after the last tile).
+  uint16_t* const stage = PERSIST ? QO + wave * 32 * D
+                                  : (wave < 2 ? K0 : wave < 4 ? K1 : wave < 6 ? V0 : V1) + (wave & 1) * 32 * D;
+
+  // The wave's 32 query rows of tile lid into its staging area: copy i brings
+  // rows 4 i .. 4 i + 3, lane l the chunk that belongs in slot l & 15 of row
+  // 4 i + (l >> 4).  Rows past Lq read as zero.  Exactly 8 copies a wave.
+  auto dma_q = [&](int lid) __attribute__((always_inline)) {
     int qt, bh;
     tile_of(lid, qt, bh);
-    const int row = qt * BM + wave * 32 + l32;
-    const uint16_t* qp = a.q + (size_t)(bh / a.H) * a.Lq * tok + (size_t)(bh % a.H) * D + (size_t)row * tok;
+    const int row0 = qt * BM + wave * 32;
+    const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(a.q + (size_t)(bh / a.H) * a.Lq * tok + (size_t)(bh % a.H) * D), (short)0, a.Lq * rbytes,
+        kBufferFlags);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int r = 4 * i + (lane >> 4);
+      const int off = row0 + r < a.Lq ? (row0 + r) * rbytes + stage_slot(lane & 15, r) * 16 : 0x7ffffff0;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rq, (lds_ptr)(stage + 4 * i * D), 16, off, 0, 0, 0);
+    }
+  };
+
+  // raw[s] = chunk 2 s + hi of the lane's own query row l32, from the staging area
+  auto read_q = [&](uint4 raw[8]) __attribute__((always_inline)) {
 #pragma unroll
     for (int s = 0; s < 8; ++s)
-      raw[s] = row < a.Lq ? *reinterpret_cast<const uint4*>(qp + (2 * s + hi) * 8) : make_uint4(0, 0, 0, 0);
+      raw[s] = *reinterpret_cast<const uint4*>(stage + l32 * D + stage_slot(2 * s + hi, l32) * 8);
   };
 
   // ---- Q: lane holds query qrow, d-chunks 2s + hi (s = 0..7) as MFMA B operands
@@ -548,26 +589,35 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
     }
   };
 
-  // ---- output: O = O^T / l (zero when no key is valid), LSE = m + ln l.
-  // Lane holds query qrow, d = 32 mb + 8 g + 4 hi + (0..3).  Buffer stores:
-  // lanes without a row address past the records and are dropped, so every
-  // wave issues exactly kOutStores store instructions.
+  // ---- output: O = O^T / l (zero when no key is valid), LSE = m + ln l,
+  // through the staging area.  Buffer stores: rows past Lq address past the
+  // records and are dropped, so every wave issues exactly kOutStores store
+  // instructions.
   auto store_o = [&](int ob, int oh, int orow, bool olive, bool empty) __attribute__((always_inline)) {
     const float l = wave_half_sum(lsum);
     const float inv = empty ? 0.f : 1.0f / l;
-    const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(a.o + (size_t)ob * a.Lq * tok), (short)0, a.Lq * rbytes, kBufferFlags);
-    const int obase = olive ? (orow * tok + oh * D) * 2 : 0x7ffffff0;
+    // the lane's row l32, d = 32 mb + 8 g + 4 hi .. + 3: half hi of chunk 4 mb + g
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int d = mb * 32 + 8 * g + 4 * hi;
         u32x2 pk;
         pk[0] = pack_bf16x2(oacc[mb][4 * g + 0] * inv, oacc[mb][4 * g + 1] * inv);
         pk[1] = pack_bf16x2(oacc[mb][4 * g + 2] * inv, oacc[mb][4 * g + 3] * inv);
-        __builtin_amdgcn_raw_buffer_store_b64(pk, ro, olive ? obase + d * 2 : obase, 0, 0);
+        *reinterpret_cast<u32x2*>(stage + l32 * D + stage_slot(4 * mb + g, l32) * 8 + 4 * hi) = pk;
       }
+    // whole rows out: slot lane & 15 of row 4 i + (lane >> 4) holds chunk stage_slot(lane & 15, row)
+    const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(a.o + (size_t)ob * a.Lq * tok + (size_t)oh * D), (short)0, a.Lq * rbytes, kBufferFlags);
+    const int row0 = orow - l32;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int r = 4 * i + (lane >> 4);
+      const u32x4 v = *reinterpret_cast<const u32x4*>(stage + r * D + (lane & 15) * 8);
+      const int grow = row0 + r;
+      const int off = grow < a.Lq ? grow * rbytes + stage_slot(lane & 15, r) * 16 : 0x7ffffff0;
+      __builtin_amdgcn_raw_buffer_store_b128(v, ro, off, 0, 0);
+    }
     const __amdgpu_buffer_rsrc_t rl = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(a.lse ? a.lse + ((size_t)ob * a.H + oh) * a.Lq : a.lse), (short)0, a.lse ? a.Lq * 4 : 0,
         kBufferFlags);
@@ -591,19 +641,23 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
       store_o(b, h, qrow, qlive, true);
       return;
     }
+    dma_q(lid);  // into the K/V buffers, which are free until the first copies
     if (ROPE) {
       for (int e = tid; e < a.tentries; e += NT) tab[e] = attn_table_entry(a, e);
       __syncthreads();
     }
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's query rows have landed
     {
       uint4 raw[8];
-      load_q(lid, raw);
+      read_q(raw);
       make_q(raw);
     }
+    __syncthreads();  // every wave has its queries out of the K/V buffers
     first_copies();
     __builtin_amdgcn_s_waitcnt(0);  // this wave's copies have landed in LDS
     __syncthreads();
     run_tile();
+    __syncthreads();  // every wave is done with the last V tile before the output staging
     store_o(b, h, qrow, qlive, false);
   } else {
     // XCD x owns a contiguous range of logical tiles; its workgroups stride
@@ -618,42 +672,60 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
       it_step = (int)(gridDim.x >> 3);  // the grid is a multiple of 8
     }
     if (lid >= it_end) return;
-    uint4 raw[8];
+    // The staging area holds the next tile's queries while a tile computes:
+    // they are read out at the tile boundary, the finished tile's output goes
+    // through the area, and then the queries of the tile after are copied in.
+    // Vector memory operations complete in issue order, so a wait that allows
+    // only the operations issued after a tile's first K/V copies to remain
+    // outstanding means those copies have landed.
     begin_tile(lid);
-    load_q(lid, raw);
-    if (lv > 0) first_copies();
+    dma_q(lid);
     __builtin_amdgcn_s_waitcnt(0);
+    {
+      uint4 raw[8];
+      read_q(raw);
+      make_q(raw);
+    }
+    int next = lid + it_step;
+    bool has_next = next < it_end;
+    if (lv > 0) first_copies();
+    if (has_next) {
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the query reads are done with the area
+      dma_q(next);
+      __builtin_amdgcn_s_waitcnt(wait_vm(kQueryCopies));
+    } else {
+      __builtin_amdgcn_s_waitcnt(0);
+    }
     __syncthreads();
     while (true) {
-      const int next = lid + it_step;
-      const bool has_next = next < it_end;
       const bool empty = lv == 0;
       reset_acc();
-      if (!empty) {
-        make_q(raw);
-        // the next tile's queries load while this tile computes (the first
-        // step's wait for its copies also covers these older loads)
-        if (has_next) load_q(next, raw);
-        run_tile();
-      } else if (has_next) {
-        load_q(next, raw);
-      }
-      // every wave is done with this tile's LDS; start the next tile's
-      // copies, then store this tile's output behind them
+      if (!empty) run_tile();
+      // every wave is done with this tile's K/V buffers
       __syncthreads();
       const int ob = b, oh = h, orow = qrow;
       const bool olive = qlive;
+      uint4 raw[8];
       if (has_next) {
+        __builtin_amdgcn_s_waitcnt(0);  // the next tile's query rows have landed
+        read_q(raw);
         begin_tile(next);
         if (lv > 0) first_copies();
       }
-      store_o(ob, oh, orow, olive, empty);
+      store_o(ob, oh, orow, olive, empty);  // its staging writes follow the query reads (in-order LDS)
       if (!has_next) break;
-      // vector memory operations complete in issue order: waiting until only
-      // the output stores are outstanding means the copies have landed
-      __builtin_amdgcn_s_waitcnt(kWaitCopiesBehindStores);
-      __syncthreads();
+      make_q(raw);
       lid = next;
+      next = lid + it_step;
+      has_next = next < it_end;
+      if (has_next) {
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the output reads are done with the area
+        dma_q(next);
+        __builtin_amdgcn_s_waitcnt(wait_vm(kOutStores + kQueryCopies));
+      } else {
+        __builtin_amdgcn_s_waitcnt(wait_vm(kOutStores));
+      }
+      __syncthreads();
     }
   }
 }
