@@ -18,10 +18,14 @@
 // (i, j) owns head i of the two (128 channels, 4 blocks of 32) for tokens
 // 64 j .. 64 j + 63 (2 blocks of 32): 8 accumulators.  The reduction over
 // the C input channels runs in stages of 64: each stage copies the W and x
-// tiles (256 rows x 64 channels each, 32 KB) straight from global memory into
-// LDS in MFMA operand order, double buffered, one barrier per stage; per
-// stage a wave issues 32 matrix instructions.  After the last stage the LDS
-// holds the rotary (cos, sin) table for the epilogue.
+// tiles (256 rows x 64 channels each) straight from global memory into LDS,
+// double buffered, one barrier per stage; per stage a wave issues 32 matrix
+// instructions.  In LDS a tile row (128 bytes) is followed by 16 bytes of
+// padding: every copy instruction then fetches whole rows with its lanes in
+// address order (coalesced; the pad lane repeats the row's last chunk), and
+// the operand reads (16 rows x one 16-byte chunk per 16 lanes, rows 144 bytes
+// apart) are free of bank conflicts.  After the last stage the LDS holds the
+// rotary (cos, sin) table for the epilogue.
 #include "launch.hpp"
 
 namespace vidax {
@@ -32,8 +36,11 @@ constexpr int NW = 8, NT = NW * 64;
 constexpr int BNC = 256;  // output channels per workgroup
 constexpr int BMT = 256;  // tokens per workgroup
 constexpr int BK = 64;    // input channels per stage
-constexpr int TILE = 256 * BK;  // elements of one staged tile
-constexpr int BLK = 512;        // elements per operand block (1 KB)
+constexpr int kPitch = BK + 8;    // elements per staged row: 64 channels + 16 bytes of padding
+constexpr int TILE = 256 * kPitch;  // elements of one staged tile (36 KB)
+constexpr int kCopies = TILE * 2 / 1024;  // 1 KB copy instructions per tile (36)
+static_assert(kCopies == 36, "the copy split over the waves assumes 36 copies per tile");
+static_assert(kRopeTableMax * 8 <= TILE * 2, "the rotary table must fit in one stage buffer");
 constexpr int kBufferFlags = 0x00020000;  // raw buffer, 32-bit data format
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -57,6 +64,14 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// Output staging: slot of 16-byte chunk c of staging row r (an involution in
+// c); for 16 consecutive rows and one chunk, and for 4 rows x 4 chunks aligned
+// by 4, the slots are distinct (no LDS bank conflicts).
+__device__ __forceinline__ int out_slot(int c, int r) {
+  const int x = r & 15;
+  return c ^ (((x & 3) << 2) | (x >> 2));
+}
+
 __device__ __forceinline__ float half_swap_sum(float x) {
   // lanes l and l ^ 32 hold the same token
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -64,9 +79,8 @@ __device__ __forceinline__ float half_swap_sum(float x) {
 }
 
 __global__ __launch_bounds__(NT) void qkv_proj_kernel(QkvArgs a) {
-  // tile layout (K order, as the attention kernel's keys): block 8 st + rb
-  // holds, for lane l, the 16 bytes of row 32 rb + (l & 31), input channels
-  // 16 st + 8 (l >> 5) .. + 7 of the stage
+  // tile layout: row r at element r * kPitch, 16-byte chunk c of the stage's
+  // 64 input channels at + 8 c
   __shared__ __attribute__((aligned(16))) uint16_t W0[TILE], W1[TILE], X0[TILE], X1[TILE];
   const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -92,37 +106,47 @@ __global__ __launch_bounds__(NT) void qkv_proj_kernel(QkvArgs a) {
       (void*)(a.w + (size_t)n0 * a.C), (short)0, rows_w * cbytes, kBufferFlags);
   const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(a.x + (size_t)m0 * a.C), (short)0, rows_x * cbytes, kBufferFlags);
-  // staging: wave w copies blocks 4 w .. 4 w + 3 of each tile
-  int goff[4];
+  // staging: copy j (of kCopies per tile) fills 16-byte slots 64 j .. 64 j + 63
+  // of the tile, lane l slot s = 64 j + l = row s / 9, chunk s % 9 (chunk 8 is
+  // the padding: it fetches chunk 7 again).  Waves 0..3 issue copies 5 w ..
+  // 5 w + 4, waves 4..7 copies 20 + 4 (w - 4) .. + 3.
+  const int cfirst = wave < 4 ? 5 * wave : 20 + 4 * (wave - 4);
+  const int ccount = wave < 4 ? 5 : 4;
+  int goff[5];
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int b = 4 * wave + u, st = b >> 3, rb = b & 7;
-    goff[u] = (32 * rb + l32) * cbytes + (16 * st + 8 * hi) * 2;
+  for (int u = 0; u < 5; ++u) {
+    const int sl = 64 * (cfirst + u) + lane, r = sl / 9, c = sl - 9 * r;
+    goff[u] = r * cbytes + min(c, 7) * 16;
   }
   auto stage = [&](int s, uint16_t* wb, uint16_t* xb) __attribute__((always_inline)) {
-    const int koff = s * BK * 2;
+    const int koff = __builtin_amdgcn_readfirstlane(s * BK * 2);
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int b = 4 * wave + u;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr)(wb + b * BLK), 16, goff[u] + koff, 0, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr)(xb + b * BLK), 16, goff[u] + koff, 0, 0, 0);
+    for (int u = 0; u < 5; ++u) {
+      if (u < ccount) {
+        const int j = cfirst + u;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr)(wb + j * 512), 16, goff[u], koff, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr)(xb + j * 512), 16, goff[u], koff, 0, 0);
+      }
     }
   };
 
   f32x16 acc[4][2];
 #pragma unroll
   for (int cb = 0; cb < 4; ++cb) acc[cb][0] = acc[cb][1] = f32x16{};
-  // one stage: 4 k-steps x (4 channel blocks x 2 token blocks)
+  // one stage: 4 k-steps x (4 channel blocks x 2 token blocks); the A operand
+  // of channel block cb, k-step st: row 128 wh + 32 cb + l32, chunk 2 st + hi
+  const int abase = (128 * wh + l32) * kPitch + 8 * hi;
+  const int bbase = (64 * wt + l32) * kPitch + 8 * hi;
   auto compute = [&](const uint16_t* wb, const uint16_t* xb) __attribute__((always_inline)) {
 #pragma unroll
     for (int st = 0; st < 4; ++st) {
       bf16x8 av[4], bv[2];
 #pragma unroll
       for (int cb = 0; cb < 4; ++cb)
-        av[cb] = *reinterpret_cast<const bf16x8*>(wb + (8 * st + 4 * wh + cb) * BLK + lane * 8);
+        av[cb] = *reinterpret_cast<const bf16x8*>(wb + abase + 32 * cb * kPitch + 16 * st);
 #pragma unroll
       for (int tb = 0; tb < 2; ++tb)
-        bv[tb] = *reinterpret_cast<const bf16x8*>(xb + (8 * st + 2 * wt + tb) * BLK + lane * 8);
+        bv[tb] = *reinterpret_cast<const bf16x8*>(xb + bbase + 32 * tb * kPitch + 16 * st);
 #pragma unroll
       for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
@@ -153,7 +177,7 @@ __global__ __launch_bounds__(NT) void qkv_proj_kernel(QkvArgs a) {
   // ---- epilogue.  Register i of acc[cb][tb] holds channel 32 cb + 8 (i >> 2)
   // + 4 hi + (i & 3) of the wave's head, token m0 + 64 wt + 32 tb + l32.
   const RopeParams& rp = a.rp;
-  float2* tab = reinterpret_cast<float2*>(W0);  // the stage buffers are free now (32 KB)
+  float2* tab = reinterpret_cast<float2*>(W0);  // the stage buffers are free now (36 KB)
   if (rp.enabled) {
     for (int e = tid; e < rp.n_entries; e += NT) tab[e] = rope_table_entry(rp, e);
     __syncthreads();
@@ -165,6 +189,10 @@ __global__ __launch_bounds__(NT) void qkv_proj_kernel(QkvArgs a) {
   const int chan0 = hg * D;          // first row of this head in W
 
   const float* gain = part == 0 ? a.gain_q : a.gain_k;
+  // the wave's 8 KB output staging area (32 tokens x 128 channels), in the
+  // stage buffers W1 and X0 that are free now: the results leave as whole
+  // 256-byte head rows, 4 tokens per store instruction
+  uint16_t* const ostage = (wave < 4 ? W1 : X0) + (wave & 3) * 32 * D;
 
 #pragma unroll
   for (int tb = 0; tb < 2; ++tb) {
@@ -224,17 +252,24 @@ __global__ __launch_bounds__(NT) void qkv_proj_kernel(QkvArgs a) {
           }
       }
     }
-    if (m < a.M) {
-      uint16_t* op = outp + (size_t)m * a.H * D + (size_t)head * D;
+    // the lane's token l32, channels 32 cb + 8 g + 4 hi .. + 3: half hi of chunk 4 cb + g
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb)
+    for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          uint2 pk;
-          pk.x = pack_bf16x2(acc[cb][tb][4 * g + 0], acc[cb][tb][4 * g + 1]);
-          pk.y = pack_bf16x2(acc[cb][tb][4 * g + 2], acc[cb][tb][4 * g + 3]);
-          *reinterpret_cast<uint2*>(op + 32 * cb + 8 * g + 4 * hi) = pk;
-        }
+      for (int g = 0; g < 4; ++g) {
+        uint2 pk;
+        pk.x = pack_bf16x2(acc[cb][tb][4 * g + 0], acc[cb][tb][4 * g + 1]);
+        pk.y = pack_bf16x2(acc[cb][tb][4 * g + 2], acc[cb][tb][4 * g + 3]);
+        *reinterpret_cast<uint2*>(ostage + l32 * D + out_slot(4 * cb + g, l32) * 8 + 4 * hi) = pk;
+      }
+    // whole rows out: slot lane & 15 of row 4 i + (lane >> 4) holds chunk out_slot(lane & 15, row)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int r = 4 * i + (lane >> 4);
+      const uint4 v = *reinterpret_cast<const uint4*>(ostage + r * D + (lane & 15) * 8);
+      const int mm = m0 + 64 * wt + 32 * tb + r;
+      if (mm < a.M)
+        *reinterpret_cast<uint4*>(outp + (size_t)mm * a.H * D + (size_t)head * D + out_slot(lane & 15, r) * 8) = v;
     }
   }
 }
