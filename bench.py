@@ -376,8 +376,8 @@ def cpu_baseline(w, q, k, v, lv, budget_s=12.0):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="wan13b_480p")
     ap.add_argument("--all", action="store_true", help="also time every workload (stderr + gpurun_out/bench_all.json)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
