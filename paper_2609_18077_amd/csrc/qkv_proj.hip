@@ -22,7 +22,8 @@
 // double buffered, one barrier per stage; per stage a wave issues 32 matrix
 // instructions.  In LDS a tile row (128 bytes) is followed by 16 bytes of
 // padding: every copy instruction then fetches whole rows with its lanes in
-// address order (coalesced; the pad lane repeats the row's last chunk), and
+// address order (coalesced; the pad lane reads past the buffer's records:
+// zero, no memory access), and
 // the operand reads (16 rows x one 16-byte chunk per 16 lanes, rows 144 bytes
 // apart) are free of bank conflicts.  After the last stage the LDS holds the
 // rotary (cos, sin) table for the epilogue.
@@ -108,15 +109,16 @@ __global__ __launch_bounds__(NT) void qkv_proj_kernel(QkvArgs a) {
       (void*)(a.x + (size_t)m0 * a.C), (short)0, rows_x * cbytes, kBufferFlags);
   // staging: copy j (of kCopies per tile) fills 16-byte slots 64 j .. 64 j + 63
   // of the tile, lane l slot s = 64 j + l = row s / 9, chunk s % 9 (chunk 8 is
-  // the padding: it fetches chunk 7 again).  Waves 0..3 issue copies 5 w ..
-  // 5 w + 4, waves 4..7 copies 20 + 4 (w - 4) .. + 3.
+  // the padding: its offset lies past the records, so it reads zero without
+  // a memory access).  Waves 0..3 issue copies 5 w .. 5 w + 4, waves 4..7
+  // copies 20 + 4 (w - 4) .. + 3.
   const int cfirst = wave < 4 ? 5 * wave : 20 + 4 * (wave - 4);
   const int ccount = wave < 4 ? 5 : 4;
   int goff[5];
 #pragma unroll
   for (int u = 0; u < 5; ++u) {
     const int sl = 64 * (cfirst + u) + lane, r = sl / 9, c = sl - 9 * r;
-    goff[u] = r * cbytes + min(c, 7) * 16;
+    goff[u] = c < 8 ? r * cbytes + c * 16 : 0x7ffff000;
   }
   auto stage = [&](int s, uint16_t* wb, uint16_t* xb) __attribute__((always_inline)) {
     const int koff = __builtin_amdgcn_readfirstlane(s * BK * 2);
