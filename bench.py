@@ -54,10 +54,15 @@ def algorithmic_bytes(w, lv):
 
 
 def kernel_source_digest():
+    """sha256 of what the forward kernel is built from: its sources and its
+    compiler flags (first 16 hex digits)."""
+    from paper_2609_18077_amd import build as _build
+
     h = hashlib.sha256()
     for name in ("attn_fwd.hip", "common.hpp"):
         with open(os.path.join(ROOT, "paper_2609_18077_amd", "csrc", name), "rb") as f:
             h.update(f.read())
+    h.update(" ".join(_build.HIPCC_FLAGS + _build.SOURCE_FLAGS.get("attn_fwd.hip", [])).encode())
     return h.hexdigest()[:16]
 
 
