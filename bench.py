@@ -384,7 +384,8 @@ def main():
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="wan13b_480p")
-    ap.add_argument("--all", action="store_true", help="also time every workload (stderr + gpurun_out/bench_all.json)")
+    ap.add_argument("--all", action="store_true",
+                    help="also time every workload (stderr, and under all_workloads in the JSON line)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--backward", action="store_true",
                     help="only time vidax_attn_bwd on the workload (stderr) and exit (for profiling the backward)")
@@ -397,7 +398,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the attention kernel runs whole on a single MI355X "
-              "(multi-GPU sharding is not part of this build); use --gpus 1", file=sys.stderr)
+              "(sharding across GPUs is described, not implemented); use --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -475,9 +476,6 @@ def main():
         rows.update(time_cold(inputs.WORKLOADS["cross_text"], max(10, args.steps // 2)))
         for ww in inputs.PROJ_WORKLOADS.values():
             rows.update(time_qkv_proj(ww, max(10, args.steps)))
-        os.makedirs(os.path.join(ROOT, "gpurun_out"), exist_ok=True)
-        with open(os.path.join(ROOT, "gpurun_out", "bench_all.json"), "w") as f:
-            json.dump(rows, f, indent=1)
         extra["all_workloads"] = rows
 
     cpu = None
