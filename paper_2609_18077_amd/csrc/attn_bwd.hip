@@ -36,7 +36,9 @@ constexpr int BN = 64;        // rows per streamed tile
 constexpr int NW = 8;         // waves per workgroup
 constexpr int NT = NW * 64;   // threads
 constexpr int BW = NW * 32;   // own rows per workgroup
-constexpr int TILE = BN * D;  // elements per streamed tile
+constexpr int TILE = BN * D;  // elements per streamed tile in V order
+constexpr int kRowPitch = 17 * 8;  // elements per row of a K-order tile (16 chunks + 1 padding)
+constexpr int KTILE = BN * kRowPitch;  // elements per streamed tile in K order (17 KB)
 constexpr int BLK = 512;      // elements per operand block (1 KB)
 constexpr int kBufferFlags = 0x00020000;  // raw buffer, 32-bit data format
 constexpr float kLog2e = 1.4426950408889634f;
@@ -96,24 +98,38 @@ __device__ __forceinline__ int valid_keys(const BwdArgs& a, int b) {
 }
 
 // ---- streamed tiles (64 rows of a [B, L, H, 128] tensor for one (b, h)).
-// LDS in MFMA operand order, 16 blocks of 1 KB:
-//   K order, block 2 st + blk: lane l's 16 bytes = row 32 blk + (l & 31),
-//     d = 16 st + 8 (l >> 5) .. + 7  (A operand, rows x d-step st)
+//   K order (read row-wise): row by row, each 256-byte row followed by 16
+//     bytes of padding, so that every direct copy (64 lanes x 16 bytes into
+//     consecutive slots) fetches whole rows with its lanes in address order
+//     (coalesced; the padding slot reads past the records: zero, no memory
+//     access) and the operand reads -- lane l: row 32 blk + (l & 31), chunk
+//     2 st + (l >> 5) -- fall on distinct banks (rows 17 chunks apart).
+// V order, in MFMA operand order, 16 blocks of 1 KB:
 //   V order, block 4 ks + mb, half r: lane l's 8 bytes = row
 //     16 ks + 8 r + 4 (l >> 5) + ((l & 15) >> 2), d = 32 mb + 16 ((l >> 4) & 1)
 //     + 4 (l & 3) .. + 3  (what the transposing read of lane l fetches for
 //     the A^T operand of d block mb, rows 16 ks .. 16 ks + 15)
-// Wave w copies blocks 2w, 2w + 1 of a tile; lane offsets in bytes from the
-// tile's first row:
+// V order: wave w copies blocks 2w, 2w + 1 of a tile.  K order: copy j (of
+// 17 a tile) fills 16-byte slots 64 j .. 64 j + 63, lane l slot s = 64 j + l =
+// row s / 17, chunk s % 17 (16: padding); wave 0 issues copies 0..2, wave
+// w > 0 copies 2 w + 1, 2 w + 2.  Lane offsets in bytes from the tile's first
+// row:
 struct Staging {
-  int k0, k1, v0, v1;
+  int r[3];        // K-order copies
+  int rfirst, rn;  // the wave's first K-order copy and their number
+  int v0, v1;      // V-order blocks
 };
 
 __device__ __forceinline__ Staging staging(int wave, int lane, int rbytes) {
-  const int l32 = lane & 31, hi = lane >> 5;
+  const int hi = lane >> 5;
   Staging s;
-  s.k0 = l32 * rbytes + (2 * wave + hi) * 16;
-  s.k1 = s.k0 + 32 * rbytes;
+  s.rfirst = wave == 0 ? 0 : 2 * wave + 1;
+  s.rn = wave == 0 ? 3 : 2;
+#pragma unroll
+  for (int u = 0; u < 3; ++u) {
+    const int sl = 64 * (s.rfirst + u) + lane, row = sl / 17, c = sl - 17 * row;
+    s.r[u] = c < 16 ? row * rbytes + c * 16 : 0x7ffffff0;
+  }
   const int vrow = 8 * hi + 4 * ((lane >> 4) & 1) + ((lane & 7) >> 1);
   const int vd = 16 * ((lane >> 3) & 1) + 8 * (lane & 1);
   const int b0 = 2 * wave, b1 = 2 * wave + 1;  // V blocks (ks, mb) = (b >> 2, b & 3)
@@ -135,6 +151,14 @@ __device__ __forceinline__ void copy_blocks(__amdgpu_buffer_rsrc_t rs, uint16_t*
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)(buf + (2 * wave + 1) * BLK), 16, g1, 0, 0, 0);
 }
 
+// the wave's K-order copies of a tile
+__device__ __forceinline__ void copy_rows(__amdgpu_buffer_rsrc_t rs, uint16_t* buf, const Staging& sg) {
+#pragma unroll
+  for (int u = 0; u < 3; ++u)
+    if (u < sg.rn)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)(buf + (sg.rfirst + u) * 512), 16, sg.r[u], 0, 0, 0);
+}
+
 // B operand of the wave's own row: chunks 2 s + hi (s = 0..7) of the row at
 // p (zero when !live).
 __device__ __forceinline__ void own_operand(const uint16_t* p, bool live, int hi, bf16x8 op[8]) {
@@ -150,9 +174,10 @@ __device__ __forceinline__ void own_operand(const uint16_t* p, bool live, int hi
 // K-order tile.
 __device__ __forceinline__ f32x16 rows_x_own(const uint16_t* t, const bf16x8 own[8], int blk, int lane) {
   f32x16 acc = f32x16{};
+  const uint16_t* base = t + (32 * blk + (lane & 31)) * kRowPitch + 8 * (lane >> 5);
 #pragma unroll
   for (int st = 0; st < 8; ++st) {
-    const bf16x8 a = *reinterpret_cast<const bf16x8*>(t + (2 * st + blk) * BLK + lane * 8);
+    const bf16x8 a = *reinterpret_cast<const bf16x8*>(base + 16 * st);
     acc = mfma32(a, own[st], acc);
   }
   return acc;
@@ -228,7 +253,7 @@ __global__ __launch_bounds__(256) void bwd_delta_kernel(BwdArgs a) {
 //   S^T = K Q^T, dP^T = V dO^T (K, V tiles in K order), P^T = exp2(S^T c -
 //   lse log2 e), dS^T = P^T (dP^T - D), dQ^T += K^T dS^T (K tile in V order).
 __global__ __launch_bounds__(NT) void bwd_dq_kernel(BwdArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t Kk0[TILE], Kk1[TILE], Vk0[TILE], Vk1[TILE], Kv0[TILE], Kv1[TILE];
+  __shared__ __attribute__((aligned(16))) uint16_t Kk0[KTILE], Kk1[KTILE], Vk0[KTILE], Vk1[KTILE], Kv0[TILE], Kv1[TILE];
   const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lid = logical_tile(blockIdx.x, a.nwg);
@@ -260,8 +285,8 @@ __global__ __launch_bounds__(NT) void bwd_dq_kernel(BwdArgs a) {
   auto copies = [&](int j, uint16_t* kk, uint16_t* vk, uint16_t* kv) __attribute__((always_inline)) {
     const __amdgpu_buffer_rsrc_t rk = tile_rsrc(kbh, j, lv, tok);
     const __amdgpu_buffer_rsrc_t rv = tile_rsrc(vbh, j, lv, tok);
-    copy_blocks(rk, kk, wave, sg.k0, sg.k1);
-    copy_blocks(rv, vk, wave, sg.k0, sg.k1);
+    copy_rows(rk, kk, sg);
+    copy_rows(rv, vk, sg);
     copy_blocks(rk, kv, wave, sg.v0, sg.v1);
   };
   copies(0, Kk0, Vk0, Kv0);
@@ -309,8 +334,8 @@ __global__ __launch_bounds__(NT) void bwd_dq_kernel(BwdArgs a) {
 //   Lv get P = 0 and so zero gradient.
 template <bool DK>
 __global__ __launch_bounds__(NT) void bwd_kv_kernel(BwdArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t Qk0[TILE], Qk1[TILE], Tv0[TILE], Tv1[TILE];
-  __shared__ __attribute__((aligned(16))) uint16_t Ok0[DK ? TILE : 8], Ok1[DK ? TILE : 8];
+  __shared__ __attribute__((aligned(16))) uint16_t Qk0[KTILE], Qk1[KTILE], Tv0[TILE], Tv1[TILE];
+  __shared__ __attribute__((aligned(16))) uint16_t Ok0[DK ? KTILE : 8], Ok1[DK ? KTILE : 8];
   __shared__ __attribute__((aligned(16))) float Lt[2][BN], Dt[2][BN];
   const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -344,10 +369,10 @@ __global__ __launch_bounds__(NT) void bwd_kv_kernel(BwdArgs a) {
   auto copies = [&](int t, uint16_t* qk, uint16_t* tv, uint16_t* ok, int buf) __attribute__((always_inline)) {
     const __amdgpu_buffer_rsrc_t rq = tile_rsrc(qbh, t, a.Lq, tok);
     const __amdgpu_buffer_rsrc_t ro = tile_rsrc(obh, t, a.Lq, tok);
-    copy_blocks(rq, qk, wave, sg.k0, sg.k1);
+    copy_rows(rq, qk, sg);
     if (DK) {
       copy_blocks(rq, tv, wave, sg.v0, sg.v1);
-      copy_blocks(ro, ok, wave, sg.k0, sg.k1);
+      copy_rows(ro, ok, sg);
     } else {
       copy_blocks(ro, tv, wave, sg.v0, sg.v1);
     }
