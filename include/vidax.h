@@ -175,9 +175,8 @@ vidax_status vidax_attn_fwd(const void* q, const void* k, const void* v, void* o
  * delta too); outputs must not overlap each other or any input.  Products
  * run on bf16 inputs (P and ds rounded to bf16) with fp32 accumulation.
  * Requires d == 128 (VIDAX_ERR_UNSUPPORTED otherwise); B, H, Lq, Lk >= 0.
- * Buffer offsets are 32-bit: (max(Lq, Lk) + 256) * H * d * 2 bytes (one batch
- * of a tensor plus one tile) must not exceed 2^31 - 1, VIDAX_ERR_UNSUPPORTED
- * beyond.
+ * Buffer offsets are 32-bit and relative to a 64-row tile: 64 * H * d * 2
+ * bytes must stay below 2 GiB - 4 KiB (VIDAX_ERR_UNSUPPORTED beyond).
  */
 vidax_status vidax_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout,
                             const float* lse, void* dq, void* dk, void* dv, float* delta, int32_t B, int32_t H,

@@ -174,8 +174,8 @@ vidax_status vidax_attn_bwd(const void* q, const void* k, const void* v, const v
   }
   const int64_t grid = ((int64_t)(Lq > Lk ? Lq : Lk) + 255) / 256 * B * H;
   if (grid > INT32_MAX) return VIDAX_ERR_UNSUPPORTED;
-  // 32-bit buffer offsets within one batch of a tensor, up to one tile past its end
-  if ((int64_t)((Lq > Lk ? Lq : Lk) + 256) * H * d * 2 > INT32_MAX) return VIDAX_ERR_UNSUPPORTED;
+  // buffer offsets are 32-bit and relative to a 64-row tile
+  if ((int64_t)64 * H * d * 2 > INT32_MAX - 4096) return VIDAX_ERR_UNSUPPORTED;
   if (B == 0 || H == 0 || (Lq == 0 && Lk == 0)) return VIDAX_OK;
   const hipError_t e = vidax::launch_attn_bwd((const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
                                               (const uint16_t*)o, (const uint16_t*)dout, lse, delta, (uint16_t*)dq,

@@ -145,8 +145,7 @@ def test_attn_bwd_rejects_invalid_arguments():
     assert call(B=-1) == INV
     assert call(scale=float("nan")) == INV
     assert call(d=64) == UNS
-    assert call(H=64, Lq=140000, Lk=64) == UNS  # one batch of q beyond 2 GiB
-    assert call(H=64, Lq=64, Lk=140000) == UNS  # one batch of k beyond 2 GiB
+    assert call(H=140000) == UNS              # one 64-row tile beyond 2 GiB
     assert call(dq=P) == INV                  # output aliases an input
     assert call(dk=7 * P + 1024) == INV       # outputs overlap each other
     assert call(delta=6 * P) == INV           # workspace aliases lse
