@@ -12,8 +12,9 @@
 //
 // Each kernel has the forward kernel's shape and layouts: eight waves of 32
 // own rows, tiles of 64 streamed rows copied straight into LDS (buffer loads
-// with the LDS flag) in MFMA operand order, two buffers per tile kind, one
-// barrier per tile.  The own rows' vectors (q and dO in the dq kernel, k and
+// with the LDS flag), two buffers per tile kind, one barrier per tile.  Tiles
+// read row-wise are kept as padded rows (whole-row copies, lanes in address
+// order); tiles read transposed are kept in MFMA operand order.  The own rows' vectors (q and dO in the dq kernel, k and
 // v in the dk/dv kernels) stay in registers as the B operand of
 // v_mfma_f32_32x32x16_bf16; the streamed tile is the A operand, read either
 // row-wise (K order) or transposed by ds_read_b64_tr_b16 (V order).  The
