@@ -1,13 +1,15 @@
 // Standalone 3D rotary embedding, bf16 [B, L, H, 128] -> bf16 (HBM-bound),
 // and its transpose (every pair rotated by minus its angle).
 //
-// Each workgroup first builds the (cos, sin) table of every (axis, position,
-// frequency) in LDS, then walks tokens with a grid stride.  A token's 16
-// channel chunks (16 B each) are handled by 16 consecutive lanes; a lane
-// decodes its token's (t, h, w) once, fetches the four (cos, sin) pairs of its
-// chunk, and applies them to the same chunk of every batch and head of that
-// token, so position decoding and table reads are amortised over B * H rows
-// and every global access is a 16-byte, row-contiguous load or store.
+// Workgroups walk tokens with a grid stride.  A token's 16 channel chunks
+// (16 B each) are handled by 16 consecutive lanes; a lane holds the four
+// frequencies of its chunk, decodes its token's (t, h, w) once, forms the
+// four (cos, sin) pairs, and applies them to the same chunk of every batch
+// and head of that token (four heads' loads in flight at a time), so angle
+// work is amortised over B * H rows and every global access is a 16-byte,
+// row-contiguous load or store.  Interleaved pairs compute the angles in
+// registers (no table, no barrier, so the first loads start at once);
+// half-split pairs stage rows in LDS and read a (cos, sin) table built there.
 #include "launch.hpp"
 
 namespace vidax {
@@ -29,17 +31,19 @@ __device__ __forceinline__ int pos_of_axis(int axis, int t, int h, int w) {
 
 // Interleaved pairs: all four pairs of a chunk are inside the chunk.
 __global__ __launch_bounds__(kThreads) void rope3d_interleaved(Rope3dArgs a) {
-  __shared__ float2 tab[kRopeTableMax];
   const RopeParams& rp = a.rp;
-  for (int e = threadIdx.x; e < rp.n_entries; e += kThreads) tab[e] = rope_table_entry(rp, e);
-  __syncthreads();
-
   const int c = threadIdx.x & 15;
   const size_t tok_stride = (size_t)a.H * kHeadDim;        // elements between tokens
   const size_t batch_stride = (size_t)a.L * tok_stride;    // elements between batches
   PairSlot slot[4];
+  float omega[4];
 #pragma unroll
-  for (int p = 0; p < 4; ++p) slot[p] = pair_slot(rp, 4 * c + p);
+  for (int p = 0; p < 4; ++p) {
+    slot[p] = pair_slot(rp, 4 * c + p);
+    const int base_a = slot[p].axis == 0 ? 0 : (slot[p].axis == 1 ? rp.base1 : rp.base2);
+    const int j = slot[p].base - base_a, da = 2 * slot[p].stride;
+    omega[p] = exp2f(-((float)(2 * j) / (float)da) * rp.log2_theta);
+  }
 
   for (int n = blockIdx.x * kTokensPerPass + (threadIdx.x >> 4); n < a.L; n += gridDim.x * kTokensPerPass) {
     const bool rot = n < rp.n_rot;
@@ -51,31 +55,44 @@ __global__ __launch_bounds__(kThreads) void rope3d_interleaved(Rope3dArgs a) {
       int w = r - h * rp.gw;
 #pragma unroll
       for (int p = 0; p < 4; ++p) {
-        float2 e = tab[slot[p].base + pos_of_axis(slot[p].axis, t, h, w) * slot[p].stride];
-        cs[p] = e.x;
-        sn[p] = rp.inverse ? -e.y : e.y;
+        float sv, cv;
+        sincosf((float)pos_of_axis(slot[p].axis, t, h, w) * omega[p], &sv, &cv);
+        cs[p] = cv;
+        sn[p] = rp.inverse ? -sv : sv;
       }
     }
+    // one row: rotate (or copy) the 16-byte chunk v of row offset off
+    auto put = [&](uint4 v, size_t off) {
+      if (rot) {
+        uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          float x0 = bf16lo_to_f32(wv[p]);
+          float x1 = bf16hi_to_f32(wv[p]);
+          float y0 = fmaf(x0, cs[p], -x1 * sn[p]);
+          float y1 = fmaf(x0, sn[p], x1 * cs[p]);
+          wv[p] = pack_bf16x2(y0, y1);
+        }
+        *reinterpret_cast<uint4*>(a.y + off) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+      } else if (a.x != a.y) {
+        *reinterpret_cast<uint4*>(a.y + off) = v;
+      }
+    };
     for (int b = 0; b < a.B; ++b) {
       const size_t row0 = b * batch_stride + (size_t)n * tok_stride + c * 8;
-      for (int hh = 0; hh < a.H; ++hh) {
-        const size_t off = row0 + (size_t)hh * kHeadDim;
-        uint4 v = *reinterpret_cast<const uint4*>(a.x + off);
-        if (rot) {
-          uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+      int hh = 0;
+      // four heads' loads in flight before the first use; a lane reads and
+      // writes only its own chunks, so in-place calls stay race free
+      for (; hh + 4 <= a.H; hh += 4) {
+        uint4 v[4];
 #pragma unroll
-          for (int p = 0; p < 4; ++p) {
-            float x0 = bf16lo_to_f32(wv[p]);
-            float x1 = bf16hi_to_f32(wv[p]);
-            float y0 = fmaf(x0, cs[p], -x1 * sn[p]);
-            float y1 = fmaf(x0, sn[p], x1 * cs[p]);
-            wv[p] = pack_bf16x2(y0, y1);
-          }
-          v = make_uint4(wv[0], wv[1], wv[2], wv[3]);
-          *reinterpret_cast<uint4*>(a.y + off) = v;
-        } else if (a.x != a.y) {
-          *reinterpret_cast<uint4*>(a.y + off) = v;
-        }
+        for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const uint4*>(a.x + row0 + (size_t)(hh + u) * kHeadDim);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) put(v[u], row0 + (size_t)(hh + u) * kHeadDim);
+      }
+      for (; hh < a.H; ++hh) {
+        const size_t off = row0 + (size_t)hh * kHeadDim;
+        put(*reinterpret_cast<const uint4*>(a.x + off), off);
       }
     }
   }
@@ -157,7 +174,8 @@ hipError_t launch_rope3d(const uint16_t* x, uint16_t* y, int B, int L, int H, co
                          hipStream_t stream) {
   Rope3dArgs a{x, y, B, L, H, rp};
   int tokens_groups = (L + kTokensPerPass - 1) / kTokensPerPass;
-  int grid = tokens_groups < 2048 ? tokens_groups : 2048;
+  // 4 workgroups per CU (the half-split kernel builds its table once per workgroup)
+  int grid = tokens_groups < 1024 ? tokens_groups : 1024;
   if (grid < 1) grid = 1;
   if (rp.pair_mode == 0) {
     hipLaunchKernelGGL(rope3d_interleaved, dim3(grid), dim3(kThreads), 0, stream, a);

@@ -91,12 +91,13 @@ def _rope_bound(x, ref, spec, rows):
 
 @pytest.mark.parametrize("mode", [0, 1])
 @pytest.mark.parametrize("inplace", [False, True])
-def test_rope3d_matches_oracle(mode, inplace):
+@pytest.mark.parametrize("heads", [3, 6])  # head rows are handled four at a time, then one by one
+def test_rope3d_matches_oracle(mode, inplace, heads):
     import torch
 
     grid = (3, 10, 30)  # 900 video tokens, then 100 unrotated tokens
-    x = inputs.bf16_tensor(11, 0, (2, 1000, 3, 128))
-    log(f"case rope3d mode={mode} inplace={inplace}")
+    x = inputs.bf16_tensor(11, 0, (2, 1000, heads, 128))
+    log(f"case rope3d mode={mode} inplace={inplace} heads={heads}")
     xd = to_dev(x)
     r = vx.Rope(grid=grid, dims=(44, 42, 42), theta=10000.0, pair_mode=mode)
     y = vx.rope3d(xd, r, out=xd if inplace else None)
