@@ -3,9 +3,10 @@
 // 3D rotation (interleaved pairs), rounding to bf16.
 //
 // Layout as in the standalone rotary kernel: the 16 channel chunks (16 B)
-// of a (token, head) row go to 16 consecutive lanes; a lane decodes its
-// token's (t, h, w) once, fetches the four (cos, sin) pairs of its chunk and
-// handles that chunk for every batch and head of the token.  A row's sum of
+// of a (token, head) row go to 16 consecutive lanes; a lane holds the four
+// frequencies of its chunk, decodes its token's (t, h, w) once, forms the four
+// (cos, sin) pairs in registers and handles that chunk for every batch and
+// head of the token, four heads' loads in flight at a time.  A row's sum of
 // squares is combined across its 16 lanes with data-parallel lane moves
 // (rotations within the 16-lane row, then permutations within quads), so
 // each lane ends with the row total without touching LDS.  Every lane reads
@@ -39,12 +40,7 @@ __device__ __forceinline__ float row16_sum(float v) {
 
 template <bool ROPE>
 __global__ __launch_bounds__(kThreads) void qk_norm_kernel(QkNormArgs a) {
-  __shared__ float2 tab[ROPE ? kRopeTableMax : 1];
   const RopeParams& rp = a.rp;
-  if (ROPE) {
-    for (int e = threadIdx.x; e < rp.n_entries; e += kThreads) tab[e] = rope_table_entry(rp, e);
-    __syncthreads();
-  }
 
   const int c = threadIdx.x & 15;  // chunk: channels 8c .. 8c + 7 = pairs 4c .. 4c + 3
   float g[8];
@@ -57,9 +53,15 @@ __global__ __launch_bounds__(kThreads) void qk_norm_kernel(QkNormArgs a) {
     g[4] = g1.x; g[5] = g1.y; g[6] = g1.z; g[7] = g1.w;
   }
   PairSlot slot[4];
+  float omega[4];  // frequency of each pair of the chunk
   if (ROPE) {
 #pragma unroll
-    for (int p = 0; p < 4; ++p) slot[p] = pair_slot(rp, 4 * c + p);
+    for (int p = 0; p < 4; ++p) {
+      slot[p] = pair_slot(rp, 4 * c + p);
+      const int base_a = slot[p].axis == 0 ? 0 : (slot[p].axis == 1 ? rp.base1 : rp.base2);
+      const int j = slot[p].base - base_a, da = 2 * slot[p].stride;
+      omega[p] = exp2f(-((float)(2 * j) / (float)da) * rp.log2_theta);
+    }
   }
   const size_t tok_stride = (size_t)a.H * kHeadDim;      // elements between tokens
   const size_t batch_stride = (size_t)a.L * tok_stride;  // elements between batches
@@ -76,16 +78,11 @@ __global__ __launch_bounds__(kThreads) void qk_norm_kernel(QkNormArgs a) {
 #pragma unroll
       for (int p = 0; p < 4; ++p) {
         const int pos = slot[p].axis == 0 ? t : (slot[p].axis == 1 ? h : w);
-        const float2 e = tab[slot[p].base + pos * slot[p].stride];
-        cs[p] = e.x;
-        sn[p] = e.y;
+        sincosf((float)pos * omega[p], &sn[p], &cs[p]);
       }
     }
-    for (int b = 0; b < a.B; ++b) {
-      const size_t row0 = b * batch_stride + (size_t)n * tok_stride + c * 8;
-      for (int hh = 0; hh < a.H; ++hh) {
-        const size_t off = row0 + (size_t)hh * kHeadDim;
-        const uint4 v = *reinterpret_cast<const uint4*>(a.x + off);
+    // one row: normalise, scale, rotate and store the 16-byte chunk v
+    auto put = [&](uint4 v, size_t off) {
         const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
         float xf[8];
         float ss = 0.f;
@@ -105,6 +102,20 @@ __global__ __launch_bounds__(kThreads) void qk_norm_kernel(QkNormArgs a) {
           o[p] = rot ? pack_bf16x2(fmaf(y0, cs[p], -y1 * sn[p]), fmaf(y0, sn[p], y1 * cs[p])) : pack_bf16x2(y0, y1);
         }
         *reinterpret_cast<uint4*>(a.y + off) = make_uint4(o[0], o[1], o[2], o[3]);
+    };
+    for (int b = 0; b < a.B; ++b) {
+      const size_t row0 = b * batch_stride + (size_t)n * tok_stride + c * 8;
+      int hh = 0;
+      for (; hh + 4 <= a.H; hh += 4) {
+        uint4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const uint4*>(a.x + row0 + (size_t)(hh + u) * kHeadDim);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) put(v[u], row0 + (size_t)(hh + u) * kHeadDim);
+      }
+      for (; hh < a.H; ++hh) {
+        const size_t off = row0 + (size_t)hh * kHeadDim;
+        put(*reinterpret_cast<const uint4*>(a.x + off), off);
       }
     }
   }
@@ -116,7 +127,7 @@ hipError_t launch_qk_norm(const uint16_t* x, uint16_t* y, const float* gain, flo
                           const RopeParams& rp, hipStream_t stream) {
   QkNormArgs a{x, y, gain, eps, B, L, H, rp};
   int groups = (L + kTokensPerPass - 1) / kTokensPerPass;
-  int grid = groups < 2048 ? groups : 2048;
+  int grid = groups < 1024 ? groups : 1024;  // 4 workgroups per CU
   if (grid < 1) grid = 1;
   if (rp.enabled)
     hipLaunchKernelGGL(qk_norm_kernel<true>, dim3(grid), dim3(kThreads), 0, stream, a);

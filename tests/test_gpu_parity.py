@@ -152,14 +152,15 @@ def _head_scaled(seed, shape, exps):
 
 @pytest.mark.parametrize("rotate,with_gain,inplace", [(False, False, False), (False, True, False),
                                                      (True, True, False), (True, False, True)])
-def test_qk_norm_rope_matches_oracle(rotate, with_gain, inplace):
+@pytest.mark.parametrize("heads", [3, 6])  # head rows are handled four at a time, then one by one
+def test_qk_norm_rope_matches_oracle(rotate, with_gain, inplace, heads):
     import torch
 
     grid = (3, 10, 30)  # 900 video tokens, then 100 unrotated tokens
-    x = _head_scaled(12, (2, 1000, 3, 128), [-6, 0, 5])
+    x = _head_scaled(12, (2, 1000, heads, 128), [-6, 0, 5, 2, -3, 1][:heads])
     g = np.random.default_rng(13).uniform(0.5, 1.5, 128).astype(np.float32)
     eps = 1e-6
-    log(f"case qk_norm_rope rotate={rotate} gain={with_gain} inplace={inplace}")
+    log(f"case qk_norm_rope rotate={rotate} gain={with_gain} inplace={inplace} heads={heads}")
     xd = to_dev(x)
     gd = torch.from_numpy(g).cuda() if with_gain else None
     r = vx.Rope(grid=grid, dims=(44, 42, 42), theta=10000.0) if rotate else None
