@@ -232,6 +232,32 @@ def test_ragged_and_edge_shapes(w):
     _full_case(w)
 
 
+def _random_shapes(n=16, seed=2026):
+    """Seeded random shapes between the hand-picked ones: batches, heads,
+    query and key counts off the tile grid, a rotated prefix (grid no larger
+    than either sequence) or none, per-batch valid lengths from 0 to past Lk,
+    raw or RMS-normalised q and k."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        B, H = int(rng.integers(1, 4)), int(rng.integers(1, 5))
+        Lq, Lk = int(rng.integers(1, 1201)), int(rng.integers(1, 1201))
+        grid = None
+        if rng.random() < 0.6:
+            t, h, w = int(rng.integers(1, 4)), int(rng.integers(1, 11)), int(rng.integers(1, 41))
+            if t * h * w <= min(Lq, Lk):
+                grid = (t, h, w)
+        kv = ("fixed", [int(x) for x in rng.integers(0, Lk + 50, B)]) if rng.random() < 0.5 else None
+        cases.append(inputs.custom(f"random{i}", B=B, H=H, Lq=Lq, Lk=Lk, seed=100 + i, grid=grid, kv_valid=kv,
+                                   rms_norm_qk=bool(rng.random() < 0.5)))
+    return cases
+
+
+@pytest.mark.parametrize("w", _random_shapes(), ids=lambda w: w.name)
+def test_random_shapes(w):
+    _full_case(w)
+
+
 @pytest.mark.parametrize("w", RAGGED[:3], ids=lambda w: w.name)
 def test_naive_kernel_agrees(w):
     _full_case(w, impl=vx.attn_fwd_naive)
