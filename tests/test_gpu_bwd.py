@@ -124,6 +124,26 @@ def test_attn_bwd_matches_oracle(w):
     _bwd_case(w)
 
 
+def _random_bwd_shapes(n=10, seed=2027):
+    """Seeded random shapes: batches, heads, query and key counts off the
+    256-row and 64-row tile grids, per-batch valid lengths from 0 to past Lk
+    or none, raw or RMS-normalised q and k."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        B, H = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+        Lq, Lk = int(rng.integers(1, 900)), int(rng.integers(1, 900))
+        kv = ("fixed", [int(x) for x in rng.integers(0, Lk + 50, B)]) if rng.random() < 0.5 else None
+        cases.append(inputs.custom(f"bwd_random{i}", B=B, H=H, Lq=Lq, Lk=Lk, seed=200 + i, kv_valid=kv,
+                                   rms_norm_qk=bool(rng.random() < 0.5)))
+    return cases
+
+
+@pytest.mark.parametrize("w", _random_bwd_shapes(), ids=lambda w: w.name)
+def test_attn_bwd_random_shapes(w):
+    _bwd_case(w)
+
+
 @pytest.mark.parametrize("scale", [0.0, -0.05, 0.3])
 def test_attn_bwd_scale_values(scale):
     _bwd_case(inputs.custom("bwd_scale", B=1, H=2, Lq=300, Lk=200, seed=38), scale=scale)
