@@ -55,6 +55,25 @@ def test_na3d_matches_oracle(w):
     _case(w)
 
 
+def _random_na_shapes(n=10, seed=2028):
+    """Seeded random grids (ragged query blocks in every axis), odd windows of
+    1 to 11 per axis, either border reading."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        grid = (int(rng.integers(1, 9)), int(rng.integers(1, 17)), int(rng.integers(1, 25)))
+        window = tuple(int(2 * rng.integers(0, 6) + 1) for _ in range(3))
+        border = "shift" if rng.random() < 0.5 else "clip"
+        cases.append(inputs.NaWorkload(f"na_random{i}", B=int(rng.integers(1, 3)), H=int(rng.integers(1, 3)),
+                                       grid=grid, seed=300 + i, window=window, border=border))
+    return cases
+
+
+@pytest.mark.parametrize("w", _random_na_shapes(), ids=lambda w: w.name)
+def test_na3d_random_shapes(w):
+    _case(w)
+
+
 @pytest.mark.parametrize("scale", [0.0, -0.2, 0.5])
 def test_na3d_scale_values(scale):
     _case(inputs.NaWorkload("na_scale", B=1, H=2, grid=(4, 6, 9), seed=81, window=(3, 5, 7)), scale=scale)
