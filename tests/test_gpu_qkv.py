@@ -106,6 +106,28 @@ PROJ = [
 ]
 
 
+def _random_proj_shapes(n=8, seed=2029):
+    """Seeded random shapes: token counts off the 256-token tile, head counts
+    that half-fill a channel tile, 1 to 6 stages of 64 input channels, a
+    rotated prefix or none, with or without bias and gains."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        B, L, H = int(rng.integers(1, 3)), int(rng.integers(1, 700)), int(rng.integers(1, 6))
+        grid = None
+        if rng.random() < 0.6:
+            t, h, w = int(rng.integers(1, 3)), int(rng.integers(1, 6)), int(rng.integers(1, 30))
+            if t * h * w <= L:
+                grid = (t, h, w)
+        cases.append(inputs.ProjWorkload(f"qkv_random{i}", B=B, L=L, H=H, C=64 * int(rng.integers(1, 7)),
+                                         seed=400 + i, grid=grid, bias=bool(rng.random() < 0.7),
+                                         gains=bool(rng.random() < 0.7)))
+    return cases
+
+
+PROJ += _random_proj_shapes()
+
+
 @pytest.mark.parametrize("w", PROJ, ids=lambda w: w.name)
 def test_qkv_proj_matches_oracle(w):
     log(f"case qkv {w.name} B{w.B} L{w.L} H{w.H} C{w.C} grid={w.grid}")
