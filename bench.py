@@ -53,16 +53,20 @@ def algorithmic_bytes(w, lv):
     return float(2 * w.B * w.Lq * row + 2 * int(lvs.sum()) * row)
 
 
+FWD_SOURCES = ("attn_fwd.hip", "xattn_fwd.hip", "attn_tile.hpp", "common.hpp")
+
+
 def kernel_source_digest():
-    """sha256 of what the forward kernel is built from: its sources and its
+    """sha256 of what the forward kernels are built from: their sources and
     compiler flags (first 16 hex digits)."""
     from paper_2609_18077_amd import build as _build
 
     h = hashlib.sha256()
-    for name in ("attn_fwd.hip", "common.hpp"):
+    for name in FWD_SOURCES:
         with open(os.path.join(ROOT, "paper_2609_18077_amd", "csrc", name), "rb") as f:
             h.update(f.read())
-    h.update(" ".join(_build.HIPCC_FLAGS + _build.SOURCE_FLAGS.get("attn_fwd.hip", [])).encode())
+    for name in FWD_SOURCES:
+        h.update(" ".join(_build.HIPCC_FLAGS + _build.SOURCE_FLAGS.get(name, [])).encode())
     return h.hexdigest()[:16]
 
 

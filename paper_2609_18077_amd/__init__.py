@@ -161,8 +161,9 @@ def rope3d_transpose(x, rope: Rope, out=None, stream=None):
     return y
 
 
-def attn_bwd(q, k, v, o, dout, lse, scale=None, kv_valid_len=None, stream=None):
-    """(dq, dk, dv) of attention without rotation, from the forward's o and lse."""
+def attn_bwd(q, k, v, o, dout, lse, scale=None, kv_valid_len=None, stream=None, out=None):
+    """(dq, dk, dv) of attention without rotation, from the forward's o and lse;
+    `out` = (dq, dk, dv) tensors to write into instead of new ones."""
     import torch
 
     for n, t in (("q", q), ("k", k), ("v", v), ("o", o), ("dout", dout)):
@@ -179,7 +180,14 @@ def attn_bwd(q, k, v, o, dout, lse, scale=None, kv_valid_len=None, stream=None):
         if kv_valid_len.dtype != torch.int32 or not kv_valid_len.is_cuda or kv_valid_len.numel() != B:
             raise ValueError("kv_valid_len must be an int32 device tensor of B elements")
         kv_valid_len = kv_valid_len.contiguous()
-    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    if out is None:
+        dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    else:
+        dq, dk, dv = out
+        for n, t, ref in (("dq", dq, q), ("dk", dk, k), ("dv", dv, v)):
+            _check_bshd(n, t)
+            if t.shape != ref.shape:
+                raise ValueError(f"{n} must have shape {tuple(ref.shape)}")
     delta = torch.empty((B, H, Lq), dtype=torch.float32, device=q.device)
     _check("vidax_attn_bwd", lib().vidax_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(dout), _ptr(lse), _ptr(dq),
                                                   _ptr(dk), _ptr(dv), _ptr(delta), B, H, Lq, Lk, d, float(scale),

@@ -442,22 +442,26 @@ hipError_t launch_attn_bwd(const uint16_t* q, const uint16_t* k, const uint16_t*
   a.B = B; a.H = H; a.Lq = Lq; a.Lk = Lk;
   a.scale = scale;
   a.c = scale * kLog2e;
+  hipError_t e = hipSuccess;
   if (Lq > 0) {
     const long rows = (long)B * Lq * H;
     long g = (rows + 15) / 16;
     if (g > 4096) g = 4096;
-    hipLaunchKernelGGL(bwd_delta_kernel, dim3((unsigned)g), dim3(256), 0, stream, a);
+    e = launch_kernel(bwd_delta_kernel, (unsigned)g, 256u, stream, a);
+    if (e != hipSuccess) return e;
     a.ntile = (Lq + BW - 1) / BW;
     a.nwg = a.ntile * B * H;
-    hipLaunchKernelGGL(bwd_dq_kernel, dim3((unsigned)a.nwg), dim3(NT), 0, stream, a);
+    e = launch_kernel(bwd_dq_kernel, (unsigned)a.nwg, (unsigned)NT, stream, a);
+    if (e != hipSuccess) return e;
   }
   if (Lk > 0) {
     a.ntile = (Lk + BW - 1) / BW;
     a.nwg = a.ntile * B * H;
-    hipLaunchKernelGGL(bwd_kv_kernel<false>, dim3((unsigned)a.nwg), dim3(NT), 0, stream, a);
-    hipLaunchKernelGGL(bwd_kv_kernel<true>, dim3((unsigned)a.nwg), dim3(NT), 0, stream, a);
+    e = launch_kernel(bwd_kv_kernel<false>, (unsigned)a.nwg, (unsigned)NT, stream, a);
+    if (e != hipSuccess) return e;
+    e = launch_kernel(bwd_kv_kernel<true>, (unsigned)a.nwg, (unsigned)NT, stream, a);
   }
-  return hipGetLastError();
+  return e;
 }
 
 }  // namespace vidax

@@ -54,23 +54,26 @@
 // a lane holds one query.
 //
 // LDS (per workgroup): K and V tiles 2 x 16 KB each, stored in MFMA operand
-// order (see below); rotary table <= 32 KB; the persistent form adds a 64 KB
-// query/output staging buffer (the plain form stages in the K/V buffers).
+// order (see below); rotary table <= 32 KB; query/output staging in the K/V
+// buffers (free before the first copies and after the last tile).
+//
+// Short key sequences without rotation (text cross-attention) go to the
+// persistent short-key kernel instead (xattn_fwd.hip).
 #include <type_traits>
 
+#include "attn_tile.hpp"
 #include "launch.hpp"
 
 namespace vidax {
 namespace {
+
+using namespace tile;
 
 constexpr int D = kHeadDim;
 constexpr int BM = 256;
 constexpr int BN = 64;
 constexpr int NW = 8;
 constexpr int NT = NW * 64;
-constexpr float kSumLimit = 18446744073709551616.0f;  // 2^64
-constexpr int kBufferFlags = 0x00020000;  // raw buffer, 32-bit data format
-
 struct AttnArgs {
   const uint16_t* q;
   const uint16_t* k;
@@ -89,33 +92,6 @@ struct AttnArgs {
   uint32_t pos_step;  // packed (t, h, w) increment of BN tokens
   uint32_t pos_sent;  // packed identity position (gt, gh, gw)
 };
-
-typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-}
-
-__device__ __forceinline__ float wave_half_max(float x) {
-  // lanes l and l^32 hold the same query: combine their partial maxima
-  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-
-__device__ __forceinline__ float wave_half_sum(float x) {
-  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
-__device__ __forceinline__ i16x4 lds_read_tr16(const uint16_t* p) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p));
-}
-
-__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
-  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c, false);
-}
 
 // Rotates one interleaved bf16 pair (x0 low, x1 high) by (cos, sin) in fp32.
 __device__ __forceinline__ uint32_t rotate_pair(uint32_t x, float2 cs) {
@@ -169,14 +145,6 @@ __device__ __forceinline__ float2 table_entry(const float2* tab, const PairIdx& 
   return *reinterpret_cast<const float2*>(reinterpret_cast<const char*>(tab) + off);
 }
 
-// Slot of 16-byte chunk c of staging row r (an involution in c).  For any 16
-// consecutive rows and one chunk, and for any 4 rows x 4 chunks aligned by 4,
-// the slots are distinct, so the staging accesses are free of bank conflicts.
-__device__ __forceinline__ int stage_slot(int c, int r) {
-  const int x = r & 15;
-  return c ^ (((x & 3) << 2) | (x >> 2));
-}
-
 __device__ __forceinline__ uint32_t packed_pos(const AttnArgs& a, int n) {
   if (n >= a.rp.n_rot) return a.pos_sent;
   const int t = n / (a.rp.gh * a.rp.gw);
@@ -198,36 +166,19 @@ __device__ __forceinline__ uint32_t packed_pos(const AttnArgs& a, int n) {
 // block is filled by one direct 1 KB global -> LDS copy.
 constexpr int TILE = BN * D;  // elements per K or V tile
 constexpr int BLK = 512;      // elements per operand block
-constexpr int kOutStores = 9;  // store instructions per wave for one tile's output (O and LSE)
-// s_waitcnt immediate: at most n vector memory operations outstanding (expcnt
-// and lgkmcnt not waited for)
-constexpr int wait_vm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
-constexpr int kQueryCopies = 8;  // staging copies per wave for one tile's queries
-#ifndef VIDAX_SHORT_KEYS
-#define VIDAX_SHORT_KEYS 2048
-#endif
-constexpr int kAttnShortKeys = VIDAX_SHORT_KEYS;  // Lk at or below which the persistent form is used
-
-typedef __attribute__((address_space(3))) void* lds_ptr;
+// Short key sequences without rotation: at or below this many keys (and with
+// enough query tiles to fill the chip) the persistent short-key kernel runs.
+constexpr int kAttnShortKeys = 2048;
 
 // ROPE: rotate the queries (and build the table); ROPE_K: also rotate the keys
 // while staging them (false when the caller passes pre-rotated keys).
-// PERSIST: one workgroup per CU loops over query tiles; the next tile's
-// queries are loaded while the current tile computes, and a finished tile's
-// output is stored after the next tile's K/V copies have been issued, so that
-// neither the query loads nor the output stores stall the pipeline (short key
-// sequences, where they are a large share of a tile's time).
-template <bool ROPE, bool ROPE_K, bool PERSIST>
+template <bool ROPE, bool ROPE_K>
 __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
-  static_assert(!(PERSIST && ROPE), "the persistent form serves unrotated attention");
   // Two K and two V buffers, each its own LDS object so that the compiler can
   // tell the direct copies into one buffer from the operand reads of another
   // (and does not wait for the copies before those reads).
   __shared__ __attribute__((aligned(16))) uint16_t K0[TILE], K1[TILE], V0[TILE], V1[TILE];
   __shared__ float2 tab[ROPE ? kAttnTableMax : 1];
-  // The persistent form copies the next tile's K/V while it stores the
-  // finished tile's output, so its query/output staging has its own buffer.
-  __shared__ __attribute__((aligned(16))) uint16_t QO[PERSIST ? NW * 32 * D : 1];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -244,17 +195,10 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   const uint16_t* kbh = a.k;
   const uint16_t* vbh = a.v;
   // Tile order: the query tiles of one (b, h) are consecutive (the K/V
-  // stream of that head is then shared in L2); the persistent form instead
-  // runs the heads of one query tile together, so that the rows its
-  // workgroups read and write at the same time are whole tokens of Q and O.
+  // stream of that head is then shared in L2).
   auto tile_of = [&](int lid, int& qt, int& bh) __attribute__((always_inline)) {
-    if (PERSIST) {
-      qt = lid / (a.B * a.H);
-      bh = lid - qt * (a.B * a.H);
-    } else {
-      qt = lid % a.nqt;
-      bh = lid / a.nqt;
-    }
+    qt = lid % a.nqt;
+    bh = lid / a.nqt;
   };
   auto begin_tile = [&](int lid) __attribute__((always_inline)) {
     int qt, bh;
@@ -275,10 +219,9 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   // wave moves one 256-byte row (coalesced), and the wave's 8 KB staging area
   // in LDS (32 rows x 16 chunks of 16 bytes, chunk c of row r at slot
   // stage_slot(c, r)) converts between that layout and the operand layout in
-  // which a lane holds one query.  The plain form borrows the K/V buffers
-  // (free before the first copies and after the last tile).
-  uint16_t* const stage = PERSIST ? QO + wave * 32 * D
-                                  : (wave < 2 ? K0 : wave < 4 ? K1 : wave < 6 ? V0 : V1) + (wave & 1) * 32 * D;
+  // which a lane holds one query.  It borrows the K/V buffers (free before
+  // the first copies and after the last tile).
+  uint16_t* const stage = (wave < 2 ? K0 : wave < 4 ? K1 : wave < 6 ? V0 : V1) + (wave & 1) * 32 * D;
 
   // The wave's 32 query rows of tile lid into its staging area: copy i brings
   // rows 4 i .. 4 i + 3, lane l the chunk that belongs in slot l & 15 of row
@@ -625,109 +568,39 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(lse), rl, olive && hi == 0 ? orow * 4 : 0x7ffffff0, 0, 0);
   };
 
-  if constexpr (!PERSIST) {
-    // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
-    // contiguous range of logical tiles so the query tiles of one (b, h)
-    // share that XCD's L2 for the K/V stream.
-    int lid;
-    {
-      const int i = blockIdx.x, n = a.nwg;
-      const int per = n >> 3, rem = n & 7, xcd = i & 7, kk = i >> 3;
-      lid = xcd < rem ? xcd * (per + 1) + kk : rem * (per + 1) + (xcd - rem) * per + kk;
-    }
-    begin_tile(lid);
-    reset_acc();
-    if (lv == 0) {  // no valid key: O = 0, LSE = -inf
-      store_o(b, h, qrow, qlive, true);
-      return;
-    }
-    dma_q(lid);  // into the K/V buffers, which are free until the first copies
-    if (ROPE) {
-      for (int e = tid; e < a.tentries; e += NT) tab[e] = attn_table_entry(a, e);
-      __syncthreads();
-    }
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's query rows have landed
-    {
-      uint4 raw[8];
-      read_q(raw);
-      make_q(raw);
-    }
-    __syncthreads();  // every wave has its queries out of the K/V buffers
-    first_copies();
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's copies have landed in LDS
-    __syncthreads();
-    run_tile();
-    __syncthreads();  // every wave is done with the last V tile before the output staging
-    store_o(b, h, qrow, qlive, false);
-  } else {
-    // XCD x owns a contiguous range of logical tiles; its workgroups stride
-    // through it together, so the heads of a query tile run at the same time.
-    int lid, it_end, it_step;
-    {
-      const int i = blockIdx.x, n = a.nwg;
-      const int per = n >> 3, rem = n & 7, xcd = i & 7, kk = i >> 3;
-      const int start = xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per;
-      lid = start + kk;
-      it_end = start + per + (xcd < rem ? 1 : 0);
-      it_step = (int)(gridDim.x >> 3);  // the grid is a multiple of 8
-    }
-    if (lid >= it_end) return;
-    // The staging area holds the next tile's queries while a tile computes:
-    // they are read out at the tile boundary, the finished tile's output goes
-    // through the area, and then the queries of the tile after are copied in.
-    // Vector memory operations complete in issue order, so a wait that allows
-    // only the operations issued after a tile's first K/V copies to remain
-    // outstanding means those copies have landed.
-    begin_tile(lid);
-    dma_q(lid);
-    __builtin_amdgcn_s_waitcnt(0);
-    {
-      uint4 raw[8];
-      read_q(raw);
-      make_q(raw);
-    }
-    int next = lid + it_step;
-    bool has_next = next < it_end;
-    if (lv > 0) first_copies();
-    if (has_next) {
-      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the query reads are done with the area
-      dma_q(next);
-      __builtin_amdgcn_s_waitcnt(wait_vm(kQueryCopies));
-    } else {
-      __builtin_amdgcn_s_waitcnt(0);
-    }
-    __syncthreads();
-    while (true) {
-      const bool empty = lv == 0;
-      reset_acc();
-      if (!empty) run_tile();
-      // every wave is done with this tile's K/V buffers
-      __syncthreads();
-      const int ob = b, oh = h, orow = qrow;
-      const bool olive = qlive;
-      uint4 raw[8];
-      if (has_next) {
-        __builtin_amdgcn_s_waitcnt(0);  // the next tile's query rows have landed
-        read_q(raw);
-        begin_tile(next);
-        if (lv > 0) first_copies();
-      }
-      store_o(ob, oh, orow, olive, empty);  // its staging writes follow the query reads (in-order LDS)
-      if (!has_next) break;
-      make_q(raw);
-      lid = next;
-      next = lid + it_step;
-      has_next = next < it_end;
-      if (has_next) {
-        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the output reads are done with the area
-        dma_q(next);
-        __builtin_amdgcn_s_waitcnt(wait_vm(kOutStores + kQueryCopies));
-      } else {
-        __builtin_amdgcn_s_waitcnt(wait_vm(kOutStores));
-      }
-      __syncthreads();
-    }
+  // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
+  // contiguous range of logical tiles so the query tiles of one (b, h)
+  // share that XCD's L2 for the K/V stream.
+  int lid;
+  {
+    const int i = blockIdx.x, n = a.nwg;
+    const int per = n >> 3, rem = n & 7, xcd = i & 7, kk = i >> 3;
+    lid = xcd < rem ? xcd * (per + 1) + kk : rem * (per + 1) + (xcd - rem) * per + kk;
   }
+  begin_tile(lid);
+  reset_acc();
+  if (lv == 0) {  // no valid key: O = 0, LSE = -inf
+    store_o(b, h, qrow, qlive, true);
+    return;
+  }
+  dma_q(lid);  // into the K/V buffers, which are free until the first copies
+  if (ROPE) {
+    for (int e = tid; e < a.tentries; e += NT) tab[e] = attn_table_entry(a, e);
+    __syncthreads();
+  }
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's query rows have landed
+  {
+    uint4 raw[8];
+    read_q(raw);
+    make_q(raw);
+  }
+  __syncthreads();  // every wave has its queries out of the K/V buffers
+  first_copies();
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's copies have landed in LDS
+  __syncthreads();
+  run_tile();
+  __syncthreads();  // every wave is done with the last V tile before the output staging
+  store_o(b, h, qrow, qlive, false);
 }
 
 }  // namespace
@@ -777,18 +650,14 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
     a.pos_sent = ((uint32_t)rp.gt << 22) | ((uint32_t)rp.gh << 11) | (uint32_t)rp.gw;
   }
   // short key sequences without rotation: one persistent workgroup per CU
+  // (the per-workgroup scan over the batch lengths bounds B)
   const int cus = cu_count();
-  const bool persist = !rp.enabled && Lk <= kAttnShortKeys && nwg > 4L * cus;
+  if (!rp.enabled && Lk <= kAttnShortKeys && nwg > 4L * cus && B <= 4096)
+    return launch_xattn_fwd(q, k, v, o, lse, B, H, Lq, Lk, scale, kv_valid_len, cus, stream);
   if (rp.enabled && !rp.keys_prerotated)
-    hipLaunchKernelGGL((attn_fwd_kernel<true, true, false>), dim3((unsigned)nwg), dim3(NT), 0, stream, a);
-  else if (rp.enabled)
-    hipLaunchKernelGGL((attn_fwd_kernel<true, false, false>), dim3((unsigned)nwg), dim3(NT), 0, stream, a);
-  else if (persist)
-    hipLaunchKernelGGL((attn_fwd_kernel<false, false, true>), dim3((unsigned)(8 * ((cus + 7) / 8))), dim3(NT), 0,
-                       stream, a);
-  else
-    hipLaunchKernelGGL((attn_fwd_kernel<false, false, false>), dim3((unsigned)nwg), dim3(NT), 0, stream, a);
-  return hipGetLastError();
+    return launch_kernel(attn_fwd_kernel<true, true>, (unsigned)nwg, (unsigned)NT, stream, a);
+  if (rp.enabled) return launch_kernel(attn_fwd_kernel<true, false>, (unsigned)nwg, (unsigned)NT, stream, a);
+  return launch_kernel(attn_fwd_kernel<false, false>, (unsigned)nwg, (unsigned)NT, stream, a);
 }
 
 }  // namespace vidax

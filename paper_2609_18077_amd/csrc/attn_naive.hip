@@ -135,8 +135,7 @@ hipError_t launch_attn_naive(const uint16_t* q, const uint16_t* k, const uint16_
   NaiveArgs a{q, k, v, o, lse, kv_valid_len, B, H, Lq, Lk, scale, rp};
   const long nqb = (Lq + kQ - 1) / kQ;
   const long grid = nqb * B * H;
-  hipLaunchKernelGGL(attn_naive_kernel, dim3((unsigned)grid), dim3(kQ), 0, stream, a);
-  return hipGetLastError();
+  return launch_kernel(attn_naive_kernel, (unsigned)grid, (unsigned)kQ, stream, a);
 }
 
 }  // namespace vidax

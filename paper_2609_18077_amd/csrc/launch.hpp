@@ -8,6 +8,16 @@
 
 // All pointers are device pointers; sizes already validated.
 namespace vidax {
+
+// Enqueues kernel(arg) on `stream` and returns the status of this launch
+// alone (an error left behind by an earlier, unrelated HIP call is not
+// reported as this launch's failure, as hipGetLastError would).
+template <typename A>
+inline hipError_t launch_kernel(void (*kernel)(A), unsigned grid, unsigned block, hipStream_t stream, A arg) {
+  void* args[] = {&arg};
+  return hipLaunchKernel(reinterpret_cast<const void*>(kernel), dim3(grid), dim3(block), args, 0, stream);
+}
+
 hipError_t launch_rope3d(const uint16_t* x, uint16_t* y, int B, int L, int H, const RopeParams& rp,
                          hipStream_t stream);
 hipError_t launch_attn_bwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, const uint16_t* o,
@@ -26,6 +36,11 @@ hipError_t launch_na3d_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
 hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o,
                            float* lse, int B, int H, int Lq, int Lk, float scale,
                            const int32_t* kv_valid_len, const RopeParams& rp, hipStream_t stream);
+// Short unrotated key sequences (text cross-attention): one persistent
+// workgroup per CU (`cus` compute units).
+hipError_t launch_xattn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o, float* lse,
+                            int B, int H, int Lq, int Lk, float scale, const int32_t* kv_valid_len, int cus,
+                            hipStream_t stream);
 hipError_t launch_qkv_proj(const uint16_t* x, const uint16_t* w, const float* bias, const float* gain_q,
                            const float* gain_k, float eps, uint16_t* q, uint16_t* k, uint16_t* v, int B, int L, int H,
                            int C, const RopeParams& rp, hipStream_t stream);

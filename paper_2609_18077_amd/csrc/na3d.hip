@@ -352,8 +352,7 @@ hipError_t launch_na3d_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
   a.nbh = (Hp + QH * WH - 1) / (QH * WH);
   a.nbw = (Wp + QW * WW - 1) / (QW * WW);
   a.nwg = B * H * a.nbt * a.nbh * a.nbw;
-  hipLaunchKernelGGL(na3d_fwd_kernel, dim3((unsigned)a.nwg), dim3(NT), 0, stream, a);
-  return hipGetLastError();
+  return launch_kernel(na3d_fwd_kernel, (unsigned)a.nwg, (unsigned)NT, stream, a);
 }
 
 }  // namespace vidax

@@ -129,11 +129,8 @@ hipError_t launch_qk_norm(const uint16_t* x, uint16_t* y, const float* gain, flo
   int groups = (L + kTokensPerPass - 1) / kTokensPerPass;
   int grid = groups < 1024 ? groups : 1024;  // 4 workgroups per CU
   if (grid < 1) grid = 1;
-  if (rp.enabled)
-    hipLaunchKernelGGL(qk_norm_kernel<true>, dim3(grid), dim3(kThreads), 0, stream, a);
-  else
-    hipLaunchKernelGGL(qk_norm_kernel<false>, dim3(grid), dim3(kThreads), 0, stream, a);
-  return hipGetLastError();
+  return rp.enabled ? launch_kernel(qk_norm_kernel<true>, (unsigned)grid, (unsigned)kThreads, stream, a)
+                    : launch_kernel(qk_norm_kernel<false>, (unsigned)grid, (unsigned)kThreads, stream, a);
 }
 
 }  // namespace vidax

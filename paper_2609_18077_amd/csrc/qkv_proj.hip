@@ -290,8 +290,7 @@ hipError_t launch_qkv_proj(const uint16_t* x, const uint16_t* w, const float* bi
   a.ntm = (a.M + BMT - 1) / BMT;
   a.nwg = a.ntn * a.ntm;
   a.rp = rp;
-  hipLaunchKernelGGL(qkv_proj_kernel, dim3((unsigned)a.nwg), dim3(NT), 0, stream, a);
-  return hipGetLastError();
+  return launch_kernel(qkv_proj_kernel, (unsigned)a.nwg, (unsigned)NT, stream, a);
 }
 
 }  // namespace vidax

@@ -177,12 +177,8 @@ hipError_t launch_rope3d(const uint16_t* x, uint16_t* y, int B, int L, int H, co
   // 4 workgroups per CU (the half-split kernel builds its table once per workgroup)
   int grid = tokens_groups < 1024 ? tokens_groups : 1024;
   if (grid < 1) grid = 1;
-  if (rp.pair_mode == 0) {
-    hipLaunchKernelGGL(rope3d_interleaved, dim3(grid), dim3(kThreads), 0, stream, a);
-  } else {
-    hipLaunchKernelGGL(rope3d_half_split, dim3(grid), dim3(kThreads), 0, stream, a);
-  }
-  return hipGetLastError();
+  return rp.pair_mode == 0 ? launch_kernel(rope3d_interleaved, (unsigned)grid, (unsigned)kThreads, stream, a)
+                           : launch_kernel(rope3d_half_split, (unsigned)grid, (unsigned)kThreads, stream, a);
 }
 
 }  // namespace vidax

@@ -91,7 +91,11 @@ vidax_status attn_common(AttnImpl impl, const void* q, const void* k, const void
   const uint64_t qbytes = (uint64_t)nq * 2, kbytes = (uint64_t)nk * 2;
   if (overlaps(o, qbytes, q, qbytes) || overlaps(o, qbytes, k, kbytes) || overlaps(o, qbytes, v, kbytes))
     return VIDAX_ERR_INVALID_ARG;
-  if (lse && (overlaps(lse, (uint64_t)B * H * Lq * 4, o, qbytes) || overlaps(lse, (uint64_t)B * H * Lq * 4, q, qbytes)))
+  // outputs (o, lse) must not overlap each other or any input (kv_valid_len included)
+  const uint64_t lbytes = lse ? (uint64_t)B * H * Lq * 4 : 0, vbytes = kv_valid_len ? (uint64_t)B * 4 : 0;
+  if (overlaps(lse, lbytes, o, qbytes) || overlaps(lse, lbytes, q, qbytes) || overlaps(lse, lbytes, k, kbytes) ||
+      overlaps(lse, lbytes, v, kbytes) || overlaps(kv_valid_len, vbytes, o, qbytes) ||
+      overlaps(kv_valid_len, vbytes, lse, lbytes))
     return VIDAX_ERR_INVALID_ARG;
   RopeParams rp = no_rope();
   if (rope) {
@@ -139,14 +143,11 @@ vidax_status rope3d_common(bool inverse, const void* x, void* y, int32_t B, int3
   return e == hipSuccess ? VIDAX_OK : VIDAX_ERR_LAUNCH;
 }
 
-}  // namespace
-
-extern "C" {
-
-vidax_status vidax_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout,
-                            const float* lse, void* dq, void* dk, void* dv, float* delta, int32_t B, int32_t H,
-                            int32_t Lq, int32_t Lk, int32_t d, float scale, const int32_t* kv_valid_len,
-                            hipStream_t stream) {
+// The backward's checks.
+vidax_status bwd_common(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                        const float* lse, void* dq, void* dk, void* dv, float* delta, int32_t B, int32_t H,
+                        int32_t Lq, int32_t Lk, int32_t d, float scale, const int32_t* kv_valid_len,
+                        hipStream_t stream) {
   if (B < 0 || H < 0 || Lq < 0 || Lk < 0 || d < 0) return VIDAX_ERR_INVALID_ARG;
   const int64_t nq = numel4(B, Lq, H, d), nk = numel4(B, Lk, H, d);
   if (nq < 0 || nk < 0) return VIDAX_ERR_INVALID_ARG;
@@ -161,13 +162,14 @@ vidax_status vidax_attn_bwd(const void* q, const void* k, const void* v, const v
   if (!isfinite(scale)) return VIDAX_ERR_INVALID_ARG;
   if (d != vidax::kHeadDim) return VIDAX_ERR_UNSUPPORTED;
   const uint64_t qb = (uint64_t)nq * 2, kb = (uint64_t)nk * 2, rb = (uint64_t)nrow * 4;
+  const uint64_t vb = kv_valid_len ? (uint64_t)B * 4 : 0;
   // outputs (dq, dk, dv, delta) must not overlap each other or any input
   const void* outs[4] = {dq, dk, dv, delta};
   const uint64_t osz[4] = {qb, kb, kb, rb};
-  const void* ins[6] = {q, k, v, o, dout, lse};
-  const uint64_t isz[6] = {qb, kb, kb, qb, qb, rb};
+  const void* ins[7] = {q, k, v, o, dout, lse, kv_valid_len};
+  const uint64_t isz[7] = {qb, kb, kb, qb, qb, rb, vb};
   for (int i = 0; i < 4; ++i) {
-    for (int j = 0; j < 6; ++j)
+    for (int j = 0; j < 7; ++j)
       if (overlaps(outs[i], osz[i], ins[j], isz[j])) return VIDAX_ERR_INVALID_ARG;
     for (int j = i + 1; j < 4; ++j)
       if (overlaps(outs[i], osz[i], outs[j], osz[j])) return VIDAX_ERR_INVALID_ARG;
@@ -177,10 +179,22 @@ vidax_status vidax_attn_bwd(const void* q, const void* k, const void* v, const v
   // buffer offsets are 32-bit and relative to a 64-row tile
   if ((int64_t)64 * H * d * 2 > INT32_MAX - 4096) return VIDAX_ERR_UNSUPPORTED;
   if (B == 0 || H == 0 || (Lq == 0 && Lk == 0)) return VIDAX_OK;
-  const hipError_t e = vidax::launch_attn_bwd((const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
-                                              (const uint16_t*)o, (const uint16_t*)dout, lse, delta, (uint16_t*)dq,
-                                              (uint16_t*)dk, (uint16_t*)dv, B, H, Lq, Lk, scale, kv_valid_len, stream);
+  const hipError_t e =
+      vidax::launch_attn_bwd((const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)o,
+                             (const uint16_t*)dout, lse, delta, (uint16_t*)dq, (uint16_t*)dk, (uint16_t*)dv, B, H, Lq,
+                             Lk, scale, kv_valid_len, stream);
   return e == hipSuccess ? VIDAX_OK : VIDAX_ERR_LAUNCH;
+}
+
+}  // namespace
+
+extern "C" {
+
+vidax_status vidax_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                            const float* lse, void* dq, void* dk, void* dv, float* delta, int32_t B, int32_t H,
+                            int32_t Lq, int32_t Lk, int32_t d, float scale, const int32_t* kv_valid_len,
+                            hipStream_t stream) {
+  return bwd_common(q, k, v, o, dout, lse, dq, dk, dv, delta, B, H, Lq, Lk, d, scale, kv_valid_len, stream);
 }
 
 vidax_status vidax_qk_norm_rope(const void* x, void* y, const float* gain, float eps, int32_t B, int32_t L, int32_t H,

@@ -1,0 +1,509 @@
+// Flash-attention forward for short key sequences without rotation (text
+// cross-attention: tens of thousands of video queries against a few hundred
+// padded text keys), gfx950, head dim 128.
+//
+// With a few key tiles per query tile, the query loads and output stores
+// (HBM) weigh as much as the products, and a kernel that streams them in and
+// out at query-tile boundaries spends most of its time waiting.  This form:
+//   * runs one persistent workgroup per CU over a contiguous run of "items"
+//     (batch, head, 256-query tile), head by head so that the K/V of a head
+//     stays in the XCD's L2; the runs are balanced by key-tile steps, not by
+//     items, because batches differ in valid length;
+//   * streams the K/V tiles through one continuous double-buffered pipeline
+//     that runs across item boundaries: the copies of the next item's first
+//     tiles are issued during the current item's last steps, and the scores
+//     of the next item's first tile are computed while the current item's
+//     last tile is turned into probabilities;
+//   * divides the memory traffic between the waves.  Waves 0-3 move queries
+//     in (direct copies into a per-wave LDS staging area) and outputs and
+//     log-sum-exps out; waves 4-7 copy the K/V tiles.  A wave's vector memory
+//     operations complete in issue order, so a wave that waits for its K/V
+//     copies every step would also wait for any query load it issued before
+//     them.  With the split, the per-step K/V wait never includes an HBM load,
+//     and the queries of item i + 1 (loaded during item i's first step) have
+//     the whole item to land.
+// All eight waves compute, 32 queries each, with the dense kernel's
+// matrix-core formulation and softmax (S^T = K Q^T, P taken from the
+// accumulator, O^T += V^T P^T through the transposing LDS read, exp2 against
+// a reference that resets only when a key block's row sum leaves [0, 2^64)).
+// The first key block of an item takes its reference from its own maximum
+// (the output is still zero) instead of computing its probabilities twice.
+//
+// LDS: K and V tiles, 2 x 16 KB each, in MFMA operand order (one 1 KB block
+// per matrix instruction operand); query/output staging 8 x 8 KB; 1 KB of
+// log-sum-exps.
+#include "attn_tile.hpp"
+#include "launch.hpp"
+
+namespace vidax {
+namespace {
+
+using namespace tile;
+
+constexpr int D = kHeadDim;
+constexpr int BM = 256;  // queries per item
+constexpr int BN = 64;   // keys per tile
+constexpr int NW = 8;
+constexpr int NT = NW * 64;
+constexpr int TILE = BN * D;  // elements of one K or V tile
+constexpr int BLK = 512;      // elements of one operand block
+constexpr int AREA = 32 * D;  // elements of one wave's staging area
+constexpr int kMemWaves = 4;
+
+// x, as a value the compiler cannot see through: offsets computed from it are
+// not hoisted out of the step loop (hoisted, every copy's uniform offsets live
+// in scalar registers for the whole loop, and those are spilled).
+__device__ __forceinline__ int opaque(int x) {
+  asm volatile("" : "+s"(x));
+  return x;
+}
+
+struct XArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  uint16_t* o;
+  float* lse;
+  const int32_t* kv_valid_len;
+  int B, H, Lq, Lk;
+  int nqt;      // items (query tiles) per (b, h)
+  float c2;     // |scale| * log2(e), or 1 when scale == 0
+  float qsign;  // +1, -1 or 0 (scale == 0) applied to the query
+};
+
+// Item coordinates: (batch b, head h, 256-query tile qt).
+struct Item {
+  int qt, h, b;
+};
+
+// Position in the flattened step stream of a workgroup: key tile j of an
+// item with nt tiles (at least 1: an item without valid keys runs one fully
+// masked tile and ends with l = 0) and lv valid keys.
+struct Step {
+  Item it;
+  int j, nt, lv;
+};
+
+__global__ __launch_bounds__(NT) void xattn_kernel(XArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t K0[TILE], K1[TILE], V0[TILE], V1[TILE];
+  __shared__ __attribute__((aligned(16))) uint16_t QO[NW * AREA];
+  __shared__ float LS[NW * 32];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool memw = wave < kMemWaves;
+  const int l32 = lane & 31;
+  const int hi = lane >> 5;
+  const int tok = a.H * D;     // elements between consecutive tokens
+  const int rbytes = tok * 2;  // bytes between consecutive tokens
+
+  // kv_valid_len through the scalar cache (a constant-address-space load), so
+  // that reading it never waits on the wave's outstanding vector memory
+  const __attribute__((address_space(4))) int32_t* lens =
+      (const __attribute__((address_space(4))) int32_t*)a.kv_valid_len;
+  auto valid_len = [&](int b) __attribute__((always_inline)) {
+    int l = a.Lk;
+    if (lens) l = min(max(lens[b], 0), a.Lk);
+    return __builtin_amdgcn_readfirstlane(l);
+  };
+  auto tiles_of = [&](int lv) __attribute__((always_inline)) { return max(1, (lv + BN - 1) / BN); };
+
+  // ---- this workgroup's run: the step stream is cut into G equal runs (at
+  // item boundaries); XCD x owns a contiguous range of runs
+  const int G = gridDim.x;  // a multiple of 8
+  const int run = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
+  const long per_batch = (long)a.H * a.nqt;
+  long total = 0;
+  for (int b = 0; b < a.B; ++b) total += per_batch * tiles_of(valid_len(b));
+  // first item whose first step is at or after step t, and that step
+  auto item_at = [&](long t, long& first_step) __attribute__((always_inline)) {
+    long cum = 0, base = 0;
+    for (int b = 0; b < a.B; ++b) {
+      const long nt = tiles_of(valid_len(b));
+      const long steps = per_batch * nt;
+      if (t < cum + steps) {
+        const long i = (t - cum + nt - 1) / nt;
+        first_step = cum + i * nt;
+        return base + i;
+      }
+      cum += steps;
+      base += per_batch;
+    }
+    first_step = cum;
+    return base;
+  };
+  long s0, s1;
+  const long lid0 = item_at(total * run / G, s0);
+  const long lid1 = item_at(total * (run + 1) / G, s1);
+  if (lid0 >= lid1) return;
+  int steps_left = (int)(s1 - s0);  // steps of the run from the current one on
+  int items_left = (int)(lid1 - lid0);
+
+  auto next_item = [&](Item& it) __attribute__((always_inline)) {
+    if (++it.qt == a.nqt) {
+      it.qt = 0;
+      if (++it.h == a.H) {
+        it.h = 0;
+        ++it.b;
+      }
+    }
+  };
+  // the next step (callers check that it lies in the run)
+  auto advance = [&](Step& c) __attribute__((always_inline)) {
+    if (++c.j == c.nt) {
+      c.j = 0;
+      const int b = c.it.b;
+      next_item(c.it);
+      if (c.it.b != b && c.it.b < a.B) {
+        c.lv = valid_len(c.it.b);
+        c.nt = tiles_of(c.lv);
+      }
+    }
+  };
+
+  // ---- queries in, outputs out (waves 0-3, each for staging areas wave and
+  // wave + 4).  Buffer records end at the last query row, so rows past Lq read
+  // as zero and their stores are dropped.  Copy i of an area brings rows
+  // 4 i .. 4 i + 3: lane l the chunk that belongs in slot l & 15 of row
+  // r = 4 i + (l >> 4), i.e. chunk stage_slot(l & 15, r) -- which depends on
+  // i only through i & 3.
+  uint16_t* const own = QO + wave * AREA;
+  int qvo[4];  // byte offset within rows 4 i .. 4 i + 3 of what this lane moves, by i & 3
+#pragma unroll
+  for (int i = 0; i < 4; ++i) qvo[i] = (lane >> 4) * rbytes + stage_slot(lane & 15, 4 * i + (lane >> 4)) * 16;
+  auto rows_rsrc = [&](const uint16_t* base, const Item& it) __attribute__((always_inline)) {
+    const int row0 = it.qt * BM;
+    return __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(base + ((size_t)it.b * a.Lq + row0) * tok + (size_t)it.h * D), (short)0,
+        __builtin_amdgcn_readfirstlane(min(a.Lq - row0, BM) * rbytes), kBufferFlags);
+  };
+  auto load_queries = [&](const Item& it) __attribute__((always_inline)) {
+    const __amdgpu_buffer_rsrc_t rq = rows_rsrc(a.q, it);
+    const int rb = opaque(rbytes), w = opaque(wave);
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int area = w + kMemWaves * t;
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rq, (lds_ptr)(QO + area * AREA + 4 * i * D), 16, qvo[i & 3],
+                                                 (area * 32 + 4 * i) * rb, 0, 0);
+    }
+  };
+  auto store_outputs = [&](const Item& it) __attribute__((always_inline)) {
+    const __amdgpu_buffer_rsrc_t ro = rows_rsrc(a.o, it);
+    const int rb = opaque(rbytes), w = opaque(wave);
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int area = w + kMemWaves * t;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const u32x4 val =
+            *reinterpret_cast<const u32x4*>(QO + area * AREA + (4 * i + (lane >> 4)) * D + (lane & 15) * 8);
+        __builtin_amdgcn_raw_buffer_store_b128(val, ro, qvo[i & 3], (area * 32 + 4 * i) * rb, 0);
+      }
+    }
+    const int row0 = it.qt * BM;
+    const __amdgpu_buffer_rsrc_t rl = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(a.lse ? a.lse + ((size_t)it.b * a.H + it.h) * a.Lq + row0 : a.lse), (short)0,
+        a.lse ? __builtin_amdgcn_readfirstlane(min(a.Lq - row0, BM) * 4) : 0, kBufferFlags);
+    const int area = wave + kMemWaves * hi;
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(LS[area * 32 + l32]), rl, (area * 32 + l32) * 4, 0, 0);
+  };
+
+  // ---- K/V copies (waves 4-7): copy wave w fills operand blocks 4 w .. 4 w + 3
+  // of the K tile and of the V tile.
+  //   K block 2 st + blk: lane l's 16 bytes = key row 32 blk + (l & 31),
+  //     d = 16 st + 8 (l >> 5) .. + 7 (A operand of S^T = K Q^T, d-step st).
+  //   V block 4 ks + mb, half r (512 bytes): lane l's 8 bytes = key row
+  //     16 ks + 8 r + 4 (l >> 5) + ((l & 15) >> 2), d = 32 mb + 16 ((l >> 4) & 1)
+  //     + 4 (l & 3) .. + 3 (what the transposing read of lane l fetches for the
+  //     V^T operand of d block mb, keys 16 ks .. 16 ks + 15).
+  // For copy wave w the K blocks 4 w + t have st = 2 w + (t >> 1), blk = t & 1,
+  // and the V blocks ks = w, mb = t: a per-lane byte offset plus a uniform one.
+  const int cw = wave & 3;
+  const int kvo = l32 * rbytes + hi * 16;
+  const int vvo = (8 * hi + 4 * ((lane >> 4) & 1) + ((lane & 7) >> 1)) * rbytes +
+                  2 * (16 * ((lane >> 3) & 1) + 8 * (lane & 1));
+  // buffer resource of a key tile: its records end at the last valid key, so
+  // rows at or past lv land in LDS as zero
+  auto tile_rsrc = [&](const uint16_t* base, const Step& c) __attribute__((always_inline)) {
+    const int rows = min(max(c.lv - c.j * BN, 0), BN);
+    return __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(base + ((size_t)c.it.b * a.Lk + (size_t)c.j * BN) * tok + (size_t)c.it.h * D), (short)0,
+        __builtin_amdgcn_readfirstlane(rows * rbytes), kBufferFlags);
+  };
+  auto copy_k = [&](const Step& c, uint16_t* buf) __attribute__((always_inline)) {
+    const __amdgpu_buffer_rsrc_t rs = tile_rsrc(a.k, c);
+    const int rb = opaque(rbytes), w = opaque(cw);
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)(buf + (4 * w + t) * BLK), 16, kvo,
+                                               32 * (t & 1) * rb + (2 * (2 * w + (t >> 1))) * 16, 0, 0);
+  };
+  auto copy_v = [&](const Step& c, uint16_t* buf) __attribute__((always_inline)) {
+    const __amdgpu_buffer_rsrc_t rs = tile_rsrc(a.v, c);
+    const int rb = opaque(rbytes), w = opaque(cw);
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)(buf + (4 * w + t) * BLK), 16, vvo,
+                                               16 * w * rb + 64 * t, 0, 0);
+  };
+
+  // ---- compute (every wave: queries l32 of its staging area, lane halves hi)
+  bf16x8 qreg[8];  // d-chunks 2 s + hi of the lane's query, MFMA B operands
+  auto read_q = [&]() __attribute__((always_inline)) {
+    const uint32_t sgn = a.qsign < 0.f ? 0x80008000u : 0u;
+    const uint32_t keep = a.qsign == 0.f ? 0u : 0xffffffffu;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      u32x4 raw = *reinterpret_cast<const u32x4*>(own + l32 * D + stage_slot(2 * s + hi, l32) * 8);
+#pragma unroll
+      for (int p = 0; p < 4; ++p) raw[p] = (raw[p] ^ sgn) & keep;
+      qreg[s] = __builtin_bit_cast(bf16x8, raw);
+    }
+  };
+
+  const int koff = lane * 8;  // per-lane element offsets of the operands (operand order)
+  const int voff = lane * 4;
+  auto qk = [&](const uint16_t* kb, f32x16 s[2]) __attribute__((always_inline)) {
+    s[0] = f32x16{};
+    s[1] = f32x16{};
+#pragma unroll
+    for (int st = 0; st < 8; ++st)
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk) {
+        const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kb + (2 * st + blk) * BLK + koff);
+        s[blk] = mfma32(kop, qreg[st], s[blk]);
+      }
+  };
+
+  f32x16 oacc[4];
+  float mref = -INFINITY;  // reference (log2 units), identical in both lane halves
+  float lsum = 0.f;        // this lane half's partial sum of p
+  auto reset_acc = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) oacc[mb] = f32x16{};
+    mref = -INFINITY;
+    lsum = 0.f;
+  };
+  const float c2 = a.c2;
+
+  // p = exp2(s c - mref) for the 32 keys of one key block as two bf16 MFMA
+  // operands; returns this lane's sum of the rounded p
+  auto softmax_p = [&](const f32x16& s, bf16x8 pop[2]) __attribute__((always_inline)) {
+    const float nm = -mref;
+    float tsum = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      uint32_t pw[4];
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[8 * ks + e], c2, nm));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[8 * ks + e + 1], c2, nm));
+        pw[e >> 1] = pack_bf16x2(p0, p1);
+        tsum = dot2(pw[e >> 1], kOnesBf16x2, tsum);
+      }
+      pop[ks] = __builtin_bit_cast(bf16x8, make_uint4(pw[0], pw[1], pw[2], pw[3]));
+    }
+    return tsum;
+  };
+  auto block_max = [&](const f32x16& s) __attribute__((always_inline)) {
+    float m = fmaxf(s[0], s[1]);
+#pragma unroll
+    for (int i = 2; i < 16; ++i) m = fmaxf(m, s[i]);
+    return wave_half_max(m) * c2;
+  };
+  // Probabilities of one key block.  The first block of an item sets the
+  // reference to its own maximum (0 when every key is masked: p = 0); a later
+  // block whose row sum of p leaves [0, 2^64) resets the reference to the
+  // running max, rescaling the output and the sum.
+  auto softmax_blk = [&](const f32x16& s, bf16x8 pop[2], bool first) __attribute__((always_inline)) {
+    if (first) {
+      const float m = block_max(s);
+      mref = m == -INFINITY ? 0.f : m;
+    }
+    float tsum = softmax_p(s, pop);
+    if (__builtin_amdgcn_ballot_w64(!(tsum < kSumLimit)) != 0) {
+      const float mnew = fmaxf(mref, block_max(s));
+      const float alpha = __builtin_amdgcn_exp2f(mref - mnew);
+      lsum *= alpha;
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) oacc[mb][i] *= alpha;
+      mref = mnew;
+      tsum = softmax_p(s, pop);
+    }
+    lsum += tsum;
+  };
+  // O^T += V^T P^T over the 32 keys of key block blk
+  auto pv_blk = [&](const uint16_t* vb, const bf16x8 pop[2], int blk) __attribute__((always_inline)) {
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+      const int ks = 2 * blk + k2;
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) {
+        const i16x4 lo = lds_read_tr16(vb + (4 * ks + mb) * BLK + voff);
+        const i16x4 hi4 = lds_read_tr16(vb + (4 * ks + mb) * BLK + BLK / 2 + voff);
+        const bf16x8 vop = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
+        oacc[mb] = mfma32(vop, pop[k2], oacc[mb]);
+      }
+    }
+  };
+  // masks keys at or past `rem` (valid keys left in this tile)
+  auto mask_tail = [&](f32x16 s[2], int rem) __attribute__((always_inline)) {
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if (blk * 32 + 8 * (i >> 2) + 4 * hi + (i & 3) >= rem) s[blk][i] = -INFINITY;
+  };
+  // O = O^T / l (zero, with lse = -inf, when l = 0: no valid key) into the
+  // wave's staging area (row l32, d = 32 mb + 8 g + 4 hi .. + 3: half hi of
+  // chunk 4 mb + g), lse = m + ln l into LS
+  auto stage_outputs = [&]() __attribute__((always_inline)) {
+    const float l = wave_half_sum(lsum);
+    const bool ok = l > 0.f;
+    const float inv = ok ? 1.0f / l : 0.f;
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        u32x2 pk;
+        pk[0] = pack_bf16x2(oacc[mb][4 * g + 0] * inv, oacc[mb][4 * g + 1] * inv);
+        pk[1] = pack_bf16x2(oacc[mb][4 * g + 2] * inv, oacc[mb][4 * g + 3] * inv);
+        *reinterpret_cast<u32x2*>(own + l32 * D + stage_slot(4 * mb + g, l32) * 8 + 4 * hi) = pk;
+      }
+    if (hi == 0) LS[wave * 32 + l32] = ok ? (mref + __log2f(l)) * 0.69314718055994531f : -INFINITY;
+  };
+
+  // ---- prologue: the first item's queries into registers, the second item's
+  // queries on their way, the first K/V tiles in LDS, the first scores
+  Step cur;
+  {
+    const int qt = (int)(lid0 % a.nqt);
+    const long bh = lid0 / a.nqt;
+    cur.it = Item{qt, (int)(bh % a.H), (int)(bh / a.H)};
+    cur.j = 0;
+    cur.lv = valid_len(cur.it.b);
+    cur.nt = tiles_of(cur.lv);
+  }
+  Step n1 = cur, n2 = cur;  // the next two steps (valid while steps_left > 1, > 2)
+  advance(n1);
+  n2 = n1;
+  advance(n2);
+  // item whose outputs are stored next; the queries loaded at the same time
+  // are those of the item two after it (valid while items_left > 1)
+  Item io = cur.it;
+  Item qnext = cur.it;
+  next_item(qnext);
+
+  if (memw) {
+    load_queries(cur.it);
+    __builtin_amdgcn_s_waitcnt(0);
+  }
+  __builtin_amdgcn_s_barrier();
+  read_q();
+  __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+  __builtin_amdgcn_s_barrier();  // every wave has its queries out of the staging area
+  if (memw && items_left > 1) load_queries(qnext);
+  if (!memw) {
+    copy_k(cur, K0);
+    if (steps_left > 1) copy_k(n1, K1);
+    copy_v(cur, V0);
+    __builtin_amdgcn_s_waitcnt(0);
+  }
+  reset_acc();
+  __builtin_amdgcn_s_barrier();
+  f32x16 sa[2], sb[2];
+  qk(K0, sa);
+  __builtin_amdgcn_s_barrier();  // step 0 refills K0
+
+  // Step (parity P = step index & 1): K of the step after next and V of the
+  // next step stream into the buffers freed by this step and the previous
+  // one; scores of the next step; probabilities and PV products of this one.
+  // of this step only the position within its item is kept
+  int jc = cur.j, ntc = cur.nt, lvc = cur.lv;
+  bool stored_any = false;  // an item has finished (its outputs wait in the staging areas)
+  auto step = [&](auto parity, f32x16 scur[2], f32x16 snext[2]) __attribute__((always_inline)) {
+    constexpr int P = decltype(parity)::value;
+    uint16_t* const kfree = P ? K1 : K0;  // held K of this step
+    uint16_t* const knext = P ? K0 : K1;  // holds K of the next step
+    uint16_t* const vcur = P ? V1 : V0;   // holds V of this step
+    uint16_t* const vfree = P ? V0 : V1;  // held V of the previous step
+    const bool first = jc == 0;
+    const bool last = jc + 1 == ntc;
+    const bool more = steps_left > 1;  // a next step exists
+    if (memw && first && stored_any) {
+      // the previous item's outputs leave; its staging areas then take the
+      // queries of the item after this one
+      store_outputs(io);
+      next_item(io);
+      __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+      if (items_left > 1) {
+        Item qn = io;
+        next_item(qn);
+        load_queries(qn);
+      }
+    }
+    if (last && more) {
+      // the next step starts the next item: its queries into registers (before
+      // this step's K/V copies are issued, so that no wait for the staged
+      // queries can include them)
+      if (memw) __builtin_amdgcn_s_waitcnt(0);
+      __builtin_amdgcn_s_barrier();
+      read_q();
+    }
+    if (!memw) {
+      if (steps_left > 2) copy_k(n2, kfree);
+      if (more) copy_v(n1, vfree);
+    }
+    if (more) qk(knext, snext);
+    if (last && lvc < (jc + 1) * BN) mask_tail(scur, lvc - jc * BN);
+    bf16x8 pop0[2], pop1[2];
+    softmax_blk(scur[0], pop0, first);
+    pv_blk(vcur, pop0, 0);
+    softmax_blk(scur[1], pop1, false);
+    pv_blk(vcur, pop1, 1);
+    if (last) {
+      stage_outputs();
+      reset_acc();
+      __builtin_amdgcn_s_waitcnt(kWaitLgkm0);  // staging writes done before the barrier
+    }
+    if (!memw) __builtin_amdgcn_s_waitcnt(0);  // this wave's K/V copies have landed
+    __builtin_amdgcn_s_barrier();
+    if (last) {
+      stored_any = true;
+      --items_left;
+    }
+    jc = n1.j;
+    ntc = n1.nt;
+    lvc = n1.lv;
+    n1 = n2;
+    advance(n2);
+    return --steps_left > 0;
+  };
+  using even = std::integral_constant<int, 0>;
+  using odd = std::integral_constant<int, 1>;
+  while (step(even(), sa, sb) && step(odd(), sb, sa)) {
+  }
+  // the last item's outputs
+  if (memw) store_outputs(io);
+}
+
+}  // namespace
+
+hipError_t launch_xattn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o, float* lse,
+                            int B, int H, int Lq, int Lk, float scale, const int32_t* kv_valid_len, int cus,
+                            hipStream_t stream) {
+  XArgs a;
+  a.q = q; a.k = k; a.v = v; a.o = o; a.lse = lse; a.kv_valid_len = kv_valid_len;
+  a.B = B; a.H = H; a.Lq = Lq; a.Lk = Lk;
+  a.nqt = (Lq + BM - 1) / BM;
+  a.c2 = scale == 0.f ? 1.f : fabsf(scale) * 1.4426950408889634f;
+  a.qsign = scale > 0.f ? 1.f : (scale < 0.f ? -1.f : 0.f);
+  return launch_kernel(xattn_kernel, (unsigned)(8 * ((cus + 7) / 8)), (unsigned)NT, stream, a);
+}
+
+}  // namespace vidax

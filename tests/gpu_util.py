@@ -16,6 +16,22 @@ MEAN_ABS = 2e-3
 REL_RMS = 1e-2
 # Natural-log sum-exp, absolute.
 LSE_ABS = 2e-2
+# Per-element bound, from the roundings the kernels make.  Each output is a
+# convex combination of value rows; the kernels round a rotated query and key
+# to bf16 before the products (score errors of a few 1e-3 in natural-log
+# units at unit-RMS inputs), round P to bf16 (relative error <= 2^-9 per
+# weight; the row sum adds the same rounded weights, so the combination stays
+# convex), accumulate in fp32 and round the output to bf16 (half an ulp).
+# The weight errors are independent across keys: the relative RMS error is
+# ~2-3e-3, and its largest element, measured against the RMS of the element's
+# (batch, head) slice, stays near 1-2% -- emulating exactly these roundings in
+# fp64 on the parity shapes gives at most 2.2%, the kernel 3.4% on the
+# 768k-element ragged rotary case.  The bound allows one ulp of the reference
+# plus 2^-4 (6.25%) of the slice RMS, about twice the worst measured; a wrong
+# value of the size of a typical output (a wrong channel, a wrong or stale
+# row, a missing tile) or an error of 10-20% on one row or channel exceeds it.
+ELEM_ULP_REL = 2.0 ** -7
+ELEM_ABS_OVER_RMS = 2.0 ** -4
 
 
 def log(*a):
@@ -67,13 +83,39 @@ def errors(got_bits: np.ndarray, ref: np.ndarray):
     }
 
 
+def element_excess(got_bits: np.ndarray, ref: np.ndarray) -> float:
+    """Largest (|got - ref| - ELEM_ULP_REL |ref|) / rms over the elements,
+    rms = RMS of the reference over the element's (batch, head) slice (all
+    compared rows, all channels); arrays are [B, rows, H, d].  A slice whose
+    reference is all zero must match exactly (returns inf otherwise)."""
+    got = oracle.bf16_bits_to_f64(got_bits)
+    worst = -np.inf
+    for b in range(ref.shape[0]):
+        for h in range(ref.shape[2]):
+            g, r = got[b, :, h], ref[b, :, h]
+            if r.size == 0:
+                continue
+            excess = np.abs(g - r) - ELEM_ULP_REL * np.abs(r)
+            rms = float(np.sqrt(np.mean(r * r)))
+            if rms == 0.0:
+                if np.any(g != 0):
+                    return np.inf
+                continue
+            worst = max(worst, float(excess.max()) / rms)
+    return worst
+
+
 def assert_parity(got_bits, ref, what=""):
+    """The contract (max-abs, mean-abs), the relative-RMS guard and the
+    per-element bound."""
     e = errors(got_bits, ref)
-    log(f"  parity {what}: {e}")
+    ex = element_excess(got_bits, ref)
+    log(f"  parity {what}: {e} element excess/rms {ex:.3e}")
     assert np.all(np.isfinite(oracle.bf16_bits_to_f64(got_bits))), what
     assert e["max_abs"] <= MAX_ABS, (what, e)
     assert e["mean_abs"] <= MEAN_ABS, (what, e)
     assert e["rel_rms"] <= REL_RMS, (what, e)
+    assert ex <= ELEM_ABS_OVER_RMS, (what, ex)
     return e
 
 

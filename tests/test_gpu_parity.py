@@ -429,7 +429,27 @@ PERSISTENT = [
 ]
 
 
-@pytest.mark.parametrize("w", PERSISTENT, ids=lambda w: w.name)
+def _random_persistent(n=6, seed=2027):
+    """Seeded random shapes that reach the short-key kernel: no rotation,
+    Lk <= 2048, ragged Lq, per-batch valid lengths (some 0, some past Lk,
+    some not a multiple of the 64-key tile) and more than 4 query tiles per
+    CU (B * H * ceil(Lq / 256) > 1024)."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        B = int(rng.integers(1, 5))
+        H = int(rng.integers(4, 17))
+        Lk = int(rng.choice([1, 63, 64, 65, 300, 512, 777, 2048]))
+        need = 1024 // (B * H) + 2  # query tiles per (b, h) beyond the threshold
+        Lq = int(rng.integers(need * 256 - 255, need * 256 + 3000))
+        lens = [int(x) for x in rng.integers(-3, Lk + 40, B)]
+        if i == 0:
+            lens[0] = 0
+        cases.append(inputs.custom(f"prand{i}", B=B, H=H, Lq=Lq, Lk=Lk, seed=300 + i, kv_valid=("fixed", lens)))
+    return cases
+
+
+@pytest.mark.parametrize("w", PERSISTENT + _random_persistent(), ids=lambda w: w.name)
 def test_persistent_short_keys_sampled(w):
     import torch
 
@@ -486,8 +506,11 @@ def test_full_size_workload_sampled(name, heads):
     del qd, kd, vd, o, l
     torch.cuda.empty_cache()
     hs = list(range(w.H)) if heads is None else heads
-    assert np.all(np.isfinite(oracle.bf16_bits_to_f64(ob[:, :, hs])))
-    assert _convex_bounds_ok(ob, v, lv, hs)
+    # every head, every row: finite and inside the convex hull of the valid value rows
+    log(f"case full-size {name}: finiteness and convex hull on all {w.H} heads")
+    for h in range(w.H):
+        assert np.all(np.isfinite(oracle.bf16_bits_to_f64(ob[:, :, h]))), h
+        assert _convex_bounds_ok(ob, v, lv, [h]), h
     rows = _sample_rows(w.Lq, np.random.default_rng(w.seed))
     log(f"case full-size {name}: oracle on {len(rows)} rows x {len(hs)} heads")
     dec = oracle.bf16_bits_to_f64

@@ -59,6 +59,11 @@ def test_attn_rejects_invalid_arguments(fn):
     assert _attn(fn, H=64, Lq=140000, Lk=64) == UNS   # one batch of q beyond 2 GiB
     assert _attn(fn, o=P) == INV                # output aliases q
     assert _attn(fn, o=2 * P + 4096) == INV     # output overlaps k
+    assert _attn(fn, lse=2 * P + 256) == INV    # lse overlaps k
+    assert _attn(fn, lse=3 * P) == INV          # lse aliases v
+    assert _attn(fn, lse=5 * P, kv=4 * P + 64) == INV        # lengths overlap o
+    assert _attn(fn, lse=5 * P, kv=5 * P + 16) == INV        # lengths overlap lse
+    assert _attn(fn, lse=5 * P, kv=6 * P, Lq=0, q=0, o=0) == 0  # no query rows: nothing to check or launch
     good = vx.Rope((1, 8, 8), (44, 42, 42)).desc()
     bad = [vx.Rope((1, 8, 8), (44, 42, 40)).desc(),     # dims do not sum to d
            vx.Rope((1, 8, 8), (43, 43, 42)).desc(),     # odd dims
@@ -125,15 +130,20 @@ def test_qk_norm_rope_rejects_invalid_arguments():
     assert call(rope=vx.Rope((2, 4, 8), (40, 42, 42)).desc()) == 1               # widths do not sum to d
 
 
-def test_attn_bwd_rejects_invalid_arguments():
+def _bwd_call():
     f = vx.lib().vidax_attn_bwd
-    INV, UNS = 1, 2
 
     def call(q=P, k=2 * P, v=3 * P, o=4 * P, do=5 * P, lse=6 * P, dq=7 * P, dk=8 * P, dv=9 * P, delta=10 * P,
              B=1, H=2, Lq=64, Lk=64, d=128, scale=0.088, kv=None):
         ptr = lambda x: ctypes.c_void_p(x) if x else None
         return f(ptr(q), ptr(k), ptr(v), ptr(o), ptr(do), ptr(lse), ptr(dq), ptr(dk), ptr(dv), ptr(delta),
                  B, H, Lq, Lk, d, scale, ptr(kv), None)
+    return call
+
+
+def test_attn_bwd_rejects_invalid_arguments():
+    INV, UNS = 1, 2
+    call = _bwd_call()
 
     assert call(q=0) == INV
     assert call(delta=0) == INV
@@ -149,6 +159,8 @@ def test_attn_bwd_rejects_invalid_arguments():
     assert call(dq=P) == INV                  # output aliases an input
     assert call(dk=7 * P + 1024) == INV       # outputs overlap each other
     assert call(delta=6 * P) == INV           # workspace aliases lse
+    assert call(kv=7 * P + 32) == INV         # lengths overlap dq
+    assert call(kv=10 * P) == INV             # lengths alias the workspace
 
 
 def test_rope3d_transpose_rejects_invalid_arguments():
