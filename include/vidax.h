@@ -25,7 +25,9 @@
  *             64-bit inside the library.
  *   Ownership the caller allocates and owns every buffer (device memory).  The
  *             library never allocates, frees or synchronises, and keeps no
- *             state between calls.  Work is enqueued on `stream`
+ *             state between calls -- except vidax_attn_bwd_noalloc, which
+ *             works in a fixed device array of the library (one per GPU,
+ *             held until the process ends) instead of a caller workspace.  Work is enqueued on `stream`
  *             (a hipStream_t; NULL = the legacy default stream).
  *   Alignment q, k, v, o, x, y must be 16-byte aligned; lse and kv_valid_len
  *             4-byte aligned.  A tensor pointer may be NULL only when that
@@ -45,13 +47,14 @@
 extern "C" {
 #endif
 
-#define VIDAX_ABI_VERSION 6
+#define VIDAX_ABI_VERSION 7
 
 typedef enum vidax_status {
   VIDAX_OK = 0,
   VIDAX_ERR_INVALID_ARG = 1,  /* null/misaligned pointer, negative size, bad descriptor */
   VIDAX_ERR_UNSUPPORTED = 2,  /* valid request outside what the kernels implement (e.g. d != 128) */
-  VIDAX_ERR_LAUNCH = 3        /* the HIP runtime rejected the launch */
+  VIDAX_ERR_LAUNCH = 3,       /* the HIP runtime rejected the launch */
+  VIDAX_ERR_TOO_LARGE = 4     /* the request exceeds a fixed device scratch size (allocation-free entry points) */
 } vidax_status;
 
 /*
@@ -182,6 +185,29 @@ vidax_status vidax_attn_bwd(const void* q, const void* k, const void* v, const v
                             const float* lse, void* dq, void* dk, void* dv, float* delta, int32_t B, int32_t H,
                             int32_t Lq, int32_t Lk, int32_t d, float scale, const int32_t* kv_valid_len,
                             hipStream_t stream);
+
+/*
+ * Allocation-free variant of vidax_attn_bwd, for callers that cannot allocate
+ * device memory or pass a workspace (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc).  Same arguments, meaning,
+ * layouts, results and errors as vidax_attn_bwd without `delta`: D lives in a
+ * fixed device array of the library (VIDAX_NOALLOC_MAX_ROWS fp32 values,
+ * 16 MiB, one copy per GPU, looked up once per device on the first call with
+ * that device current and held until the process ends).  The call itself
+ * allocates nothing.
+ *   B * H * Lq > VIDAX_NOALLOC_MAX_ROWS -> VIDAX_ERR_TOO_LARGE (nothing launched);
+ *   the device array cannot be located -> VIDAX_ERR_LAUNCH.
+ * Every call on one GPU shares that GPU's array: calls that overlap in time on
+ * one GPU (different streams, or different host threads without ordering)
+ * race and give undefined results; calls ordered on one stream are safe.
+ * The array is fully rewritten by each call before it is read (nothing needs
+ * to start at zero).
+ */
+#define VIDAX_NOALLOC_MAX_ROWS 4194304
+vidax_status vidax_attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                                    const float* lse, void* dq, void* dk, void* dv, int32_t B, int32_t H,
+                                    int32_t Lq, int32_t Lk, int32_t d, float scale, const int32_t* kv_valid_len,
+                                    hipStream_t stream);
 
 /*
  * 3D neighbourhood (windowed) attention, the attention of the LTX-2.5 VAE

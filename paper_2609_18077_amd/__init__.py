@@ -17,12 +17,14 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libvidax.so")
 
 VIDAX_OK = 0
-_STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported configuration", 3: "kernel launch failed"}
+_STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported configuration", 3: "kernel launch failed",
+           4: "request exceeds the fixed device scratch of an allocation-free entry point"}
 
 EXPORTED_SYMBOLS = (
     "vidax_rope3d",
     "vidax_rope3d_transpose",
     "vidax_attn_bwd",
+    "vidax_attn_bwd_noalloc",
     "vidax_na3d_fwd",
     "vidax_qkv_proj",
     "vidax_qk_norm_rope",
@@ -89,6 +91,8 @@ def lib() -> ctypes.CDLL:
         L.vidax_rope3d_transpose.restype = i32
         L.vidax_attn_bwd.argtypes = [vp] * 10 + [i32, i32, i32, i32, i32, f32, vp, vp]
         L.vidax_attn_bwd.restype = i32
+        L.vidax_attn_bwd_noalloc.argtypes = [vp] * 9 + [i32, i32, i32, i32, i32, f32, vp, vp]
+        L.vidax_attn_bwd_noalloc.restype = i32
         L.vidax_na3d_fwd.argtypes = [vp] * 5 + [i32] * 10 + [f32, vp]
         L.vidax_na3d_fwd.restype = i32
         L.vidax_qkv_proj.argtypes = [vp] * 5 + [f32] + [vp] * 3 + [i32] * 5 + [ctypes.POINTER(RopeDesc), vp]
@@ -161,9 +165,12 @@ def rope3d_transpose(x, rope: Rope, out=None, stream=None):
     return y
 
 
-def attn_bwd(q, k, v, o, dout, lse, scale=None, kv_valid_len=None, stream=None, out=None):
-    """(dq, dk, dv) of attention without rotation, from the forward's o and lse;
-    `out` = (dq, dk, dv) tensors to write into instead of new ones."""
+def attn_bwd(q, k, v, o, dout, lse, scale=None, kv_valid_len=None, stream=None, noalloc=False, out=None):
+    """(dq, dk, dv) of attention without rotation, from the forward's o and lse.
+
+    noalloc=True calls vidax_attn_bwd_noalloc (D in the library's fixed
+    device array instead of a workspace tensor); `out` = (dq, dk, dv) tensors
+    to write into instead of new ones."""
     import torch
 
     for n, t in (("q", q), ("k", k), ("v", v), ("o", o), ("dout", dout)):
@@ -188,6 +195,12 @@ def attn_bwd(q, k, v, o, dout, lse, scale=None, kv_valid_len=None, stream=None, 
             _check_bshd(n, t)
             if t.shape != ref.shape:
                 raise ValueError(f"{n} must have shape {tuple(ref.shape)}")
+    if noalloc:
+        _check("vidax_attn_bwd_noalloc",
+               lib().vidax_attn_bwd_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(dout), _ptr(lse), _ptr(dq),
+                                            _ptr(dk), _ptr(dv), B, H, Lq, Lk, d, float(scale), _ptr(kv_valid_len),
+                                            _stream(stream)))
+        return dq, dk, dv
     delta = torch.empty((B, H, Lq), dtype=torch.float32, device=q.device)
     _check("vidax_attn_bwd", lib().vidax_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(dout), _ptr(lse), _ptr(dq),
                                                   _ptr(dk), _ptr(dv), _ptr(delta), B, H, Lq, Lk, d, float(scale),

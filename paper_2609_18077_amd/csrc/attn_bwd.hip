@@ -27,6 +27,8 @@
 // than the 256 registers a wave has at two waves per SIMD.
 #include <type_traits>
 
+#include <mutex>
+
 #include "launch.hpp"
 
 namespace vidax {
@@ -462,6 +464,51 @@ hipError_t launch_attn_bwd(const uint16_t* q, const uint16_t* k, const uint16_t*
     e = launch_kernel(bwd_kv_kernel<true>, (unsigned)a.nwg, (unsigned)NT, stream, a);
   }
   return e;
+}
+
+// ---- allocation-free backward ------------------------------------------
+//
+// D of the allocation-free entry point lives in this fixed array instead of a
+// caller workspace: kNoAllocRows fp32 values (16 MiB), one copy per GPU the
+// library runs on, held until the process ends.  In host code `scratch` is
+// only a stand-in for the symbol; its device address (different on every
+// GPU) is looked up once per device and only that address is handed to the
+// kernels.  Calls that overlap on one GPU share the array and race; the
+// delta kernel rewrites every value a call reads, so nothing is cleared.
+static __device__ __align__(256) float scratch[kNoAllocRows];
+
+constexpr int kMaxDevices = 64;
+
+// Device address of `scratch` on the current device (looked up on the first
+// call made with that device current).
+static hipError_t scratch_address(float** out) {
+  static std::mutex mu;
+  static float* addr[kMaxDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!ptr) return hipErrorInvalidSymbol;
+    addr[dev] = static_cast<float*>(ptr);
+  }
+  *out = addr[dev];
+  return hipSuccess;
+}
+
+hipError_t launch_attn_bwd_noalloc(const uint16_t* q, const uint16_t* k, const uint16_t* v, const uint16_t* o,
+                                   const uint16_t* dout, const float* lse, uint16_t* dq, uint16_t* dk, uint16_t* dv,
+                                   int B, int H, int Lq, int Lk, float scale, const int32_t* kv_valid_len,
+                                   hipStream_t stream) {
+  if ((long)B * H * Lq > kNoAllocRows) return hipErrorInvalidValue;  // the entry point rejects this first
+  float* delta = nullptr;
+  const hipError_t e = scratch_address(&delta);
+  if (e != hipSuccess) return e;
+  return launch_attn_bwd(q, k, v, o, dout, lse, delta, dq, dk, dv, B, H, Lq, Lk, scale, kv_valid_len, stream);
 }
 
 }  // namespace vidax

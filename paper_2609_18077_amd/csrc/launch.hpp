@@ -24,6 +24,13 @@ hipError_t launch_attn_bwd(const uint16_t* q, const uint16_t* k, const uint16_t*
                            const uint16_t* dout, const float* lse, float* delta, uint16_t* dq, uint16_t* dk,
                            uint16_t* dv, int B, int H, int Lq, int Lk, float scale, const int32_t* kv_valid_len,
                            hipStream_t stream);
+// The backward with D in the library's fixed device array (allocation-free
+// entry point); B * H * Lq must not exceed kNoAllocRows.
+constexpr long kNoAllocRows = 4194304;
+hipError_t launch_attn_bwd_noalloc(const uint16_t* q, const uint16_t* k, const uint16_t* v, const uint16_t* o,
+                                   const uint16_t* dout, const float* lse, uint16_t* dq, uint16_t* dk, uint16_t* dv,
+                                   int B, int H, int Lq, int Lk, float scale, const int32_t* kv_valid_len,
+                                   hipStream_t stream);
 hipError_t launch_qk_norm(const uint16_t* x, uint16_t* y, const float* gain, float eps, int B, int L, int H,
                           const RopeParams& rp, hipStream_t stream);
 hipError_t launch_attn_naive(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o,

@@ -8,6 +8,8 @@
 #include "../../include/vidax.h"
 #include "launch.hpp"
 
+static_assert(VIDAX_NOALLOC_MAX_ROWS == vidax::kNoAllocRows, "allocation-free scratch size");
+
 namespace {
 
 using vidax::RopeParams;
@@ -143,8 +145,9 @@ vidax_status rope3d_common(bool inverse, const void* x, void* y, int32_t B, int3
   return e == hipSuccess ? VIDAX_OK : VIDAX_ERR_LAUNCH;
 }
 
-// The backward's checks.
-vidax_status bwd_common(const void* q, const void* k, const void* v, const void* o, const void* dout,
+// The backward's checks; `noalloc`: D goes to the library's fixed device
+// array (delta is ignored and must be NULL) instead of the caller's workspace.
+vidax_status bwd_common(bool noalloc, const void* q, const void* k, const void* v, const void* o, const void* dout,
                         const float* lse, void* dq, void* dk, void* dv, float* delta, int32_t B, int32_t H,
                         int32_t Lq, int32_t Lk, int32_t d, float scale, const int32_t* kv_valid_len,
                         hipStream_t stream) {
@@ -153,8 +156,9 @@ vidax_status bwd_common(const void* q, const void* k, const void* v, const void*
   if (nq < 0 || nk < 0) return VIDAX_ERR_INVALID_ARG;
   const int64_t nrow = (int64_t)B * H * Lq;  // lse, delta
   if ((nq > 0 && (!q || !o || !dout || !dq)) || (nk > 0 && (!k || !v || !dk || !dv)) ||
-      (nrow > 0 && (!lse || !delta)))
+      (nrow > 0 && (!lse || (!noalloc && !delta))))
     return VIDAX_ERR_INVALID_ARG;
+  if (noalloc && delta) return VIDAX_ERR_INVALID_ARG;
   for (const void* p : {q, k, v, o, dout, (const void*)dq, (const void*)dk, (const void*)dv})
     if (!aligned(p, 16)) return VIDAX_ERR_INVALID_ARG;
   if (!aligned(lse, 16) || !aligned(delta, 16)) return VIDAX_ERR_INVALID_ARG;
@@ -165,7 +169,7 @@ vidax_status bwd_common(const void* q, const void* k, const void* v, const void*
   const uint64_t vb = kv_valid_len ? (uint64_t)B * 4 : 0;
   // outputs (dq, dk, dv, delta) must not overlap each other or any input
   const void* outs[4] = {dq, dk, dv, delta};
-  const uint64_t osz[4] = {qb, kb, kb, rb};
+  const uint64_t osz[4] = {qb, kb, kb, delta ? rb : 0};
   const void* ins[7] = {q, k, v, o, dout, lse, kv_valid_len};
   const uint64_t isz[7] = {qb, kb, kb, qb, qb, rb, vb};
   for (int i = 0; i < 4; ++i) {
@@ -178,11 +182,15 @@ vidax_status bwd_common(const void* q, const void* k, const void* v, const void*
   if (grid > INT32_MAX) return VIDAX_ERR_UNSUPPORTED;
   // buffer offsets are 32-bit and relative to a 64-row tile
   if ((int64_t)64 * H * d * 2 > INT32_MAX - 4096) return VIDAX_ERR_UNSUPPORTED;
+  if (noalloc && nrow > vidax::kNoAllocRows) return VIDAX_ERR_TOO_LARGE;
   if (B == 0 || H == 0 || (Lq == 0 && Lk == 0)) return VIDAX_OK;
   const hipError_t e =
-      vidax::launch_attn_bwd((const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)o,
-                             (const uint16_t*)dout, lse, delta, (uint16_t*)dq, (uint16_t*)dk, (uint16_t*)dv, B, H, Lq,
-                             Lk, scale, kv_valid_len, stream);
+      noalloc ? vidax::launch_attn_bwd_noalloc((const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v,
+                                               (const uint16_t*)o, (const uint16_t*)dout, lse, (uint16_t*)dq,
+                                               (uint16_t*)dk, (uint16_t*)dv, B, H, Lq, Lk, scale, kv_valid_len, stream)
+              : vidax::launch_attn_bwd((const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)o,
+                                       (const uint16_t*)dout, lse, delta, (uint16_t*)dq, (uint16_t*)dk, (uint16_t*)dv,
+                                       B, H, Lq, Lk, scale, kv_valid_len, stream);
   return e == hipSuccess ? VIDAX_OK : VIDAX_ERR_LAUNCH;
 }
 
@@ -194,7 +202,14 @@ vidax_status vidax_attn_bwd(const void* q, const void* k, const void* v, const v
                             const float* lse, void* dq, void* dk, void* dv, float* delta, int32_t B, int32_t H,
                             int32_t Lq, int32_t Lk, int32_t d, float scale, const int32_t* kv_valid_len,
                             hipStream_t stream) {
-  return bwd_common(q, k, v, o, dout, lse, dq, dk, dv, delta, B, H, Lq, Lk, d, scale, kv_valid_len, stream);
+  return bwd_common(false, q, k, v, o, dout, lse, dq, dk, dv, delta, B, H, Lq, Lk, d, scale, kv_valid_len, stream);
+}
+
+vidax_status vidax_attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* o, const void* dout,
+                                    const float* lse, void* dq, void* dk, void* dv, int32_t B, int32_t H,
+                                    int32_t Lq, int32_t Lk, int32_t d, float scale, const int32_t* kv_valid_len,
+                                    hipStream_t stream) {
+  return bwd_common(true, q, k, v, o, dout, lse, dq, dk, dv, nullptr, B, H, Lq, Lk, d, scale, kv_valid_len, stream);
 }
 
 vidax_status vidax_qk_norm_rope(const void* x, void* y, const float* gain, float eps, int32_t B, int32_t L, int32_t H,
@@ -326,6 +341,7 @@ const char* vidax_status_string(vidax_status s) {
     case VIDAX_ERR_INVALID_ARG: return "invalid argument";
     case VIDAX_ERR_UNSUPPORTED: return "unsupported configuration";
     case VIDAX_ERR_LAUNCH: return "kernel launch failed";
+    case VIDAX_ERR_TOO_LARGE: return "request exceeds the fixed device scratch of an allocation-free entry point";
   }
   return "unknown status";
 }

@@ -25,9 +25,10 @@ def test_library_exports_every_declared_function():
     assert set(declared) == set(vx.EXPORTED_SYMBOLS), declared
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.vidax_abi_version() == 6
+    assert lib.vidax_abi_version() == 7
     for s, text in [(0, b"ok"), (1, b"invalid argument"), (2, b"unsupported configuration"), (3, b"kernel launch failed")]:
         assert lib.vidax_status_string(s) == text
+    assert b"allocation-free" in lib.vidax_status_string(4)
     assert lib.vidax_status_string(99) == b"unknown status"
 
 
@@ -130,12 +131,15 @@ def test_qk_norm_rope_rejects_invalid_arguments():
     assert call(rope=vx.Rope((2, 4, 8), (40, 42, 42)).desc()) == 1               # widths do not sum to d
 
 
-def _bwd_call():
-    f = vx.lib().vidax_attn_bwd
+def _bwd_call(noalloc=False):
+    f = vx.lib().vidax_attn_bwd_noalloc if noalloc else vx.lib().vidax_attn_bwd
 
     def call(q=P, k=2 * P, v=3 * P, o=4 * P, do=5 * P, lse=6 * P, dq=7 * P, dk=8 * P, dv=9 * P, delta=10 * P,
              B=1, H=2, Lq=64, Lk=64, d=128, scale=0.088, kv=None):
         ptr = lambda x: ctypes.c_void_p(x) if x else None
+        if noalloc:
+            return f(ptr(q), ptr(k), ptr(v), ptr(o), ptr(do), ptr(lse), ptr(dq), ptr(dk), ptr(dv),
+                     B, H, Lq, Lk, d, scale, ptr(kv), None)
         return f(ptr(q), ptr(k), ptr(v), ptr(o), ptr(do), ptr(lse), ptr(dq), ptr(dk), ptr(dv), ptr(delta),
                  B, H, Lq, Lk, d, scale, ptr(kv), None)
     return call
@@ -161,6 +165,23 @@ def test_attn_bwd_rejects_invalid_arguments():
     assert call(delta=6 * P) == INV           # workspace aliases lse
     assert call(kv=7 * P + 32) == INV         # lengths overlap dq
     assert call(kv=10 * P) == INV             # lengths alias the workspace
+
+
+def test_attn_bwd_noalloc_rejects_invalid_arguments():
+    INV, UNS, BIG = 1, 2, 4
+    call = _bwd_call(noalloc=True)
+    max_rows = 4194304  # VIDAX_NOALLOC_MAX_ROWS
+    assert call(q=0) == INV
+    assert call(lse=0) == INV
+    assert call(q=0, o=0, do=0, dq=0, lse=0, k=0, v=0, dk=0, dv=0, Lq=0, Lk=0) == 0  # empty
+    assert call(dq=7 * P + 8) == INV
+    assert call(d=64) == UNS
+    assert call(dq=P) == INV
+    assert call(kv=9 * P) == INV              # lengths alias dv
+    # beyond the fixed scratch: rejected before any HIP call
+    assert call(B=1, H=64, Lq=max_rows // 64 + 1, Lk=64) == BIG
+    assert call(B=2, H=32, Lq=max_rows // 64 + 64, Lk=64) == BIG
+    # at the limit it would launch: only checked on the GPU
 
 
 def test_rope3d_transpose_rejects_invalid_arguments():
