@@ -49,6 +49,11 @@ constexpr int TILE = BN * D;  // elements of one K or V tile
 constexpr int BLK = 512;      // elements of one operand block
 constexpr int AREA = 32 * D;  // elements of one wave's staging area
 constexpr int kMemWaves = 4;
+// Cache policy of the query loads and output stores: non-temporal.  Each
+// query row is read once and each output row written once; as streaming
+// accesses they do not displace the K/V tiles of the XCD's heads from the L2,
+// which the K/V copies hit every step (measured: cross_text 0.60 -> 0.57 ms).
+constexpr int kStreamPolicy = 2;
 
 // x, as a value the compiler cannot see through: offsets computed from it are
 // not hoisted out of the step loop (hoisted, every copy's uniform offsets live
@@ -187,7 +192,7 @@ __global__ __launch_bounds__(NT) void xattn_kernel(XArgs a) {
 #pragma unroll
       for (int i = 0; i < 8; ++i)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rq, (lds_ptr)(QO + area * AREA + 4 * i * D), 16, qvo[i & 3],
-                                                 (area * 32 + 4 * i) * rb, 0, 0);
+                                                 (area * 32 + 4 * i) * rb, 0, kStreamPolicy);
     }
   };
   auto store_outputs = [&](const Item& it) __attribute__((always_inline)) {
@@ -200,7 +205,7 @@ __global__ __launch_bounds__(NT) void xattn_kernel(XArgs a) {
       for (int i = 0; i < 8; ++i) {
         const u32x4 val =
             *reinterpret_cast<const u32x4*>(QO + area * AREA + (4 * i + (lane >> 4)) * D + (lane & 15) * 8);
-        __builtin_amdgcn_raw_buffer_store_b128(val, ro, qvo[i & 3], (area * 32 + 4 * i) * rb, 0);
+        __builtin_amdgcn_raw_buffer_store_b128(val, ro, qvo[i & 3], (area * 32 + 4 * i) * rb, kStreamPolicy);
       }
     }
     const int row0 = it.qt * BM;
