@@ -10,12 +10,17 @@ per-head RMS-normalised Q/K, inputs resident in HBM before timing starts.
 The variant that rotates both Q and K inside the attention kernel is timed
 beside it (``alt.fused_rope``).
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME] [--all]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--all] [--only-metric]
 
 Prints ONE JSON line on stdout (everything else goes to stderr).  FLOPs per
 step = 4 * B * H * Lq * Lv * d (valid keys only; exponentials, rotation and
 masking not counted).  The roofline entry is the attention kernel alone,
-timed with HIP events on the stream it is launched on.
+timed with HIP events on the stream it is launched on.  The line also carries
+every other configuration of the workload table (the attention call alone:
+ms, TFLOP/s, % of the bf16 peak, algorithmic GB/s and % of HBM, seed; the
+text cross-attention also with its inputs evicted from L2/MALL), the engine
+clock and power sampled during the timed loop, and the CPU oracle's rate with
+the host's core count and CPU model.
 """
 
 from __future__ import annotations
@@ -84,7 +89,65 @@ def traffic_from_counters(workload):
     return rec.get("hbm_bytes_per_launch")
 
 
-def time_gpu(w, steps, warmup, fused=False):
+class Telemetry:
+    """Samples the GPU's engine clock (the current level of pp_dpm_sclk) and
+    its power (hwmon power1_input) from sysfs in a background thread while a
+    timed loop runs; both stay None where the files cannot be read."""
+
+    def __init__(self, period_s=0.003):
+        import glob
+        import threading
+
+        self.period = period_s
+        dev = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        self.sclk = dev[0] if dev else None
+        hw = sorted(glob.glob(os.path.dirname(dev[0]) + "/hwmon/hwmon*/power1_input")) if dev else []
+        self.power = hw[0] if hw else None
+        self.clk, self.pw = [], []
+        self._stop = threading.Event()
+        self._t = threading.Thread(target=self._run, daemon=True)
+
+    def _read(self):
+        if self.sclk:
+            try:
+                with open(self.sclk) as f:
+                    for line in f:
+                        if line.rstrip().endswith("*"):
+                            self.clk.append(float(line.split(":")[1].strip().rstrip("*").strip().lower()
+                                                  .replace("mhz", "")))
+            except (OSError, ValueError, IndexError):
+                self.sclk = None
+        if self.power:
+            try:
+                with open(self.power) as f:
+                    self.pw.append(float(f.read()) / 1e6)
+            except (OSError, ValueError):
+                self.power = None
+
+    def _run(self):
+        while not self._stop.is_set():
+            self._read()
+            time.sleep(self.period)
+
+    def __enter__(self):
+        self._t.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        self._t.join()
+
+    def summary(self):
+        def stats(v, unit):
+            if not v:
+                return None
+            return {"mean": round(float(np.mean(v)), 1), "min": round(float(np.min(v)), 1),
+                    "max": round(float(np.max(v)), 1), "samples": len(v), "unit": unit}
+        return {"engine_clock": stats(self.clk, "MHz"), "power": stats(self.pw, "W"),
+                "source": "sysfs pp_dpm_sclk / hwmon power1_input, sampled every 3 ms during the timed loop"}
+
+
+def time_gpu(w, steps, warmup, fused=False, telemetry=False):
     """Times `steps` steps.  Events bracket the attention launch of each step
     (on the stream it runs on); the wall clock covers the whole step."""
     import dataclasses
@@ -128,6 +191,9 @@ def time_gpu(w, steps, warmup, fused=False):
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     torch.cuda.synchronize()
+    tel = Telemetry() if telemetry else None
+    if tel:
+        tel.__enter__()
     t0 = time.perf_counter()
     for i in range(steps):
         prologue()
@@ -136,6 +202,8 @@ def time_gpu(w, steps, warmup, fused=False):
         ends[i].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    if tel:
+        tel.__exit__(None, None, None)
     per = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])  # ms per attention launch
     return {
         "two_pass": two_pass,
@@ -146,6 +214,7 @@ def time_gpu(w, steps, warmup, fused=False):
         "event_ms_std": float(per.std()),
         "lv": lv,
         "inputs": (q, k, v, lv),
+        "telemetry": tel.summary() if tel else None,
     }
 
 
@@ -339,12 +408,17 @@ def environment():
     pr = torch.cuda.get_device_properties(0)
     env = {"gpu": pr.name, "arch": getattr(pr, "gcnArchName", None), "cus": pr.multi_processor_count,
            "hip": torch.version.hip, "torch": torch.__version__}
+    env["host_cpu"] = host_cpu_model()
+    env["host_cores"] = os.cpu_count()
+    return env
+
+
+def host_cpu_model():
     try:
         with open("/proc/cpuinfo") as f:
-            env["host_cpu"] = next(l.split(":", 1)[1].strip() for l in f if l.startswith("model name"))
+            return next(l.split(":", 1)[1].strip() for l in f if l.startswith("model name"))
     except (OSError, StopIteration):
-        env["host_cpu"] = None
-    return env
+        return None
 
 
 def cpu_baseline(w, q, k, v, lv, budget_s=12.0):
@@ -377,8 +451,11 @@ def cpu_baseline(w, q, k, v, lv, budget_s=12.0):
         "cores": cores,
         "kind": "oracle",
         "sample": f"fp64 oracle on {heads} of {w.H} heads of {w.name} (all {w.Lq} query rows x {w.Lk} keys), "
-                  f"{secs:.1f} s, {cores} threads",
+                  f"{secs:.1f} s, {cores} threads on a host of {os.cpu_count()} cores",
         "seconds": secs,
+        "host_cores": os.cpu_count(),
+        "threads": cores,
+        "cpu_model": host_cpu_model(),
     }
 
 
@@ -389,7 +466,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="wan13b_480p")
     ap.add_argument("--all", action="store_true",
-                    help="also time every workload (stderr, and under all_workloads in the JSON line)")
+                    help="also time the rotary, backward, neighbourhood-attention and projection kernels "
+                         "(stderr, and under all_workloads in the JSON line)")
+    ap.add_argument("--only-metric", action="store_true",
+                    help="time only the metric's workload (not the other configurations)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--backward", action="store_true",
                     help="only time vidax_attn_bwd on the workload (stderr) and exit (for profiling the backward)")
@@ -435,7 +515,7 @@ def main():
         for ww in inputs.PROJ_WORKLOADS.values():
             time_qkv_proj(ww, args.steps)
         return
-    r = time_gpu(w, args.steps, args.warmup)
+    r = time_gpu(w, args.steps, args.warmup, telemetry=True)
     q, k, v, lv = r.pop("inputs")
     fl = flops(w, lv)
     value = fl / (r["wall_ms_per_step"] * 1e-3) / 1e12
@@ -455,31 +535,38 @@ def main():
         torch.cuda.empty_cache()
 
     extra = {}
-    if args.all:
+    if not args.only_metric:
+        # every other configuration of the workload table, compact: the
+        # attention call alone (HIP events), fewer steps for the long ones
         rows = {}
         for name, ww in inputs.WORKLOADS.items():
-            rr = time_gpu(ww, max(5, args.steps // 2), 3)
+            if name == w.name:
+                continue
+            n = 5 if ww.Lq * ww.Lk * ww.H * ww.B > 2e10 else max(5, args.steps // 2)
+            rr = time_gpu(ww, n, 3)
             _, _, _, lvw = rr.pop("inputs")
             f2 = flops(ww, lvw)
             t = rr["event_ms_mean"] * 1e-3
+            gbs = algorithmic_bytes(ww, lvw) / t / 1e9
             rows[name] = {
-                "step_ms": rr["wall_ms_per_step"], "ms": rr["event_ms_mean"], "ms_median": rr["event_ms_median"], "ms_min": rr["event_ms_min"],
-                "tflops": f2 / t / 1e12, "pct_bf16_peak": 100 * f2 / t / 1e12 / PEAK_BF16_TFLOPS,
-                "algorithmic_GBs": algorithmic_bytes(ww, lvw) / t / 1e9,
-                "kv_valid_len": None if lvw is None else [int(x) for x in lvw],
+                "ms": round(rr["event_ms_mean"], 4), "ms_min": round(rr["event_ms_min"], 4), "steps": n,
+                "tflops": round(f2 / t / 1e12, 2), "pct_bf16_peak": round(100 * f2 / t / 1e12 / PEAK_BF16_TFLOPS, 2),
+                "algorithmic_GBs": round(gbs, 1), "pct_hbm_peak": round(100 * gbs / PEAK_HBM_GBS, 2),
+                "seed": ww.seed, "kv_valid_len": None if lvw is None else [int(x) for x in lvw],
             }
             log(f"[bench] {name:14s} {rows[name]['ms']:9.3f} ms  {rows[name]['tflops']:8.1f} TFLOP/s  "
-                f"{rows[name]['pct_bf16_peak']:5.1f}%  {rows[name]['algorithmic_GBs']:8.1f} GB/s")
+                f"{rows[name]['pct_bf16_peak']:5.1f}%  {gbs:8.1f} GB/s ({rows[name]['pct_hbm_peak']:.1f}% of HBM)")
             torch.cuda.empty_cache()
-        rows.update(time_prologues(inputs.WORKLOADS["wan13b_480p"], max(5, args.steps // 2)))
-        for name in ("wan13b_480p", "cross_text"):
-            rows.update(time_backward(inputs.WORKLOADS[name], max(5, args.steps // 2)))
-            torch.cuda.empty_cache()
-        for ww in inputs.NA_WORKLOADS.values():
-            rows.update(time_na3d(ww, max(10, args.steps)))
         rows.update(time_cold(inputs.WORKLOADS["cross_text"], max(10, args.steps // 2)))
-        for ww in inputs.PROJ_WORKLOADS.values():
-            rows.update(time_qkv_proj(ww, max(10, args.steps)))
+        if args.all:
+            rows.update(time_prologues(inputs.WORKLOADS["wan13b_480p"], max(5, args.steps // 2)))
+            for name in ("wan13b_480p", "cross_text"):
+                rows.update(time_backward(inputs.WORKLOADS[name], max(5, args.steps // 2)))
+                torch.cuda.empty_cache()
+            for ww in inputs.NA_WORKLOADS.values():
+                rows.update(time_na3d(ww, max(10, args.steps)))
+            for ww in inputs.PROJ_WORKLOADS.values():
+                rows.update(time_qkv_proj(ww, max(10, args.steps)))
         extra["all_workloads"] = rows
 
     cpu = None
@@ -511,6 +598,7 @@ def main():
                      if r["two_pass"] else "3d interleaved 44/42/42 theta=1e4, fused") if w.grid else None,
             "kv_valid_len": None if lv is None else [int(x) for x in lv],
             "inputs": "N(0,1) bf16, per-head RMS-normalised Q/K" if w.rms_norm_qk else "N(0,1) bf16",
+            "seed": w.seed,
             "flops_per_call": fl,
         },
         "roofline": {
@@ -528,9 +616,9 @@ def main():
         },
         "alt": alt,
         "cpu_baseline": None if cpu is None else dict(
-            {k2: cpu[k2] for k2 in ("value", "unit", "cores", "kind", "sample")},
+            {k2: cpu[k2] for k2 in ("value", "unit", "cores", "kind", "sample", "host_cores", "threads", "cpu_model")},
             gpu_over_cpu=round(achieved / cpu["value"], 1)),
-        "env": environment(),
+        "env": dict(environment(), telemetry=r["telemetry"]),
     }
     if extra:
         rec["all_workloads"] = extra["all_workloads"]
