@@ -271,8 +271,9 @@ vidax_status vidax_attn_fwd_naive(const void* q, const void* k, const void* v, v
                                   const int32_t* kv_valid_len, const vidax_rope3d_desc* rope,
                                   hipStream_t stream);
 
-/* Static string describing a status code (never NULL). */
-const char* vidax_status_string(vidax_status s);
+/* Static string describing a status code (never NULL; any int32_t value is
+ * accepted, codes that are not a vidax_status give "unknown status"). */
+const char* vidax_status_string(int32_t status);
 
 /* VIDAX_ABI_VERSION of the loaded library. */
 int32_t vidax_abi_version(void);

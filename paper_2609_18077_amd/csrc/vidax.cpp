@@ -335,8 +335,8 @@ vidax_status vidax_qkv_proj(const void* x, const void* w, const float* bias, con
   return e == hipSuccess ? VIDAX_OK : VIDAX_ERR_LAUNCH;
 }
 
-const char* vidax_status_string(vidax_status s) {
-  switch (s) {
+const char* vidax_status_string(int32_t status) {
+  switch (status) {
     case VIDAX_OK: return "ok";
     case VIDAX_ERR_INVALID_ARG: return "invalid argument";
     case VIDAX_ERR_UNSUPPORTED: return "unsupported configuration";
