@@ -25,17 +25,21 @@
 //   transposing LDS read (ds_read_b64_tr_b16), which hands each lane 4 keys
 //   of one d column per read.
 //
-// Softmax: p = exp2(s * c - m) with c = |scale| * log2 e in one FMA (the
-// rotated query is rounded to bf16 unscaled; a negative scale negates it, a
-// zero scale zeroes it).  The reference m of a row is not the running max but
-// the max of the block that last reset it: no per-tile max is computed.  A key
-// block whose row sum of p reaches 2^64 (or is not finite -- the first block
-// always is, since m starts at -inf) resets m to the running max, rescales the
-// output and sum, and recomputes its p.  p therefore never exceeds 2^64, so
-// the bf16 P, fp32 sums and fp32 output accumulators cannot overflow, and the
-// result equals the usual online softmax up to rounding.  Row sums add the
-// bf16-rounded p actually fed to the PV product (v_dot2 with ones).
-//
+// Softmax: the query is multiplied by scale * log2 e (in fp32, after the
+// rotation) and rounded to bf16 once, so the products are scores in log2
+// units; and the score accumulators of a tile start at -m instead of zero, so
+// the matrix cores hand out s - m and p = exp2 of it takes no vector
+// arithmetic besides the exponential.  The reference m of a row is not the
+// running max but the max of the block that last reset it: no per-tile max is
+// computed.  The first block of a row (its sum starts at +inf) and any key
+// block whose row sum of p reaches 2^64 or is not finite reset m to the
+// running max, rescale the output and sum, shift the scores already computed
+// from the old m (the other block of the tile, the next tile), and recompute
+// the block's p.  p therefore never exceeds 2^64, so the bf16 P, fp32 sums
+// and fp32 output accumulators cannot overflow, and the result equals the
+// usual online softmax up to rounding.  Row sums add the bf16-rounded p
+// actually fed to the PV product (v_dot2 with ones).
+
 // Rotary embedding: each workgroup builds an fp32 (cos, sin) table per (axis,
 // position, frequency) in LDS; each axis has one extra identity position used
 // by unrotated tokens.  Queries are rotated as they are loaded.  Keys either
@@ -84,8 +88,9 @@ struct AttnArgs {
   int B, H, Lq, Lk;
   int nqt;      // query tiles per (b, h)
   int nwg;      // total workgroups
-  float c2;     // |scale| * log2(e), or 1 when scale == 0
-  float qsign;  // +1, -1, or 0 (scale == 0) applied to the rotated query
+  float qmul;   // scale * log2(e): the rotated query is multiplied by it before rounding to bf16
+  float c2;     // unrotated query: |scale| * log2(e) (1 when scale == 0), applied in the exponent
+  float qsign;  // unrotated query: +1, -1 or 0 (scale == 0) applied to the query
   RopeParams rp;
   // attention rotary table: axis a holds (G_a + 1) positions x d_a/2 pairs
   int tbase1, tbase2, tentries;
@@ -252,6 +257,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   bf16x8 qreg[8];
   auto make_q = [&](const uint4 raw[8]) __attribute__((always_inline)) {
     const uint32_t qpos = ROPE ? packed_pos(a, qlive ? qrow : a.rp.n_rot) : 0u;
+    const float qm = a.qmul;
     const uint32_t sgn = a.qsign < 0.f ? 0x80008000u : 0u;
     const uint32_t keep = a.qsign == 0.f ? 0u : 0xffffffffu;
 #pragma unroll
@@ -260,8 +266,13 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
       uint32_t wq[4] = {raw[s].x, raw[s].y, raw[s].z, raw[s].w};
 #pragma unroll
       for (int p = 0; p < 4; ++p) {
-        if (ROPE) wq[p] = rotate_pair(wq[p], table_entry(tab, pair_idx(a, 4 * c + p), qpos));
-        wq[p] = (wq[p] ^ sgn) & keep;
+        if (ROPE) {  // rotated and scaled in fp32, rounded once
+          const float x0 = bf16lo_to_f32(wq[p]), x1 = bf16hi_to_f32(wq[p]);
+          const float2 cs = table_entry(tab, pair_idx(a, 4 * c + p), qpos);
+          wq[p] = pack_bf16x2(fmaf(x0, cs.x, -x1 * cs.y) * qm, fmaf(x0, cs.y, x1 * cs.x) * qm);
+        } else {  // exact: sign only
+          wq[p] = (wq[p] ^ sgn) & keep;
+        }
       }
       qreg[s] = __builtin_bit_cast(bf16x8, make_uint4(wq[0], wq[1], wq[2], wq[3]));
     }
@@ -360,43 +371,51 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   const int koff = lane * 8;
   const int voff = lane * 4;
 
+  // Rotated query (scaled into log2 units): the score accumulators start at
+  // -cbase instead of zero, so that the products come out as s - cbase with
+  // no vector work.  Unrotated query: they start at zero and p = exp2(s c2 -
+  // mref) takes one FMA (cbase stays 0).
+  float mref = -INFINITY;  // reference max (log2 units), identical in both lane halves
+  float cbase = 0.f;       // the offset the score accumulators start from (mref once finite)
+  f32x16 cneg = f32x16{};
   auto qk = [&](const uint16_t* kb, f32x16 s[2]) __attribute__((always_inline)) {
-    s[0] = f32x16{};
-    s[1] = f32x16{};
 #pragma unroll
     for (int st = 0; st < 8; ++st) {
 #pragma unroll
       for (int blk = 0; blk < 2; ++blk) {
         const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kb + (2 * st + blk) * BLK + koff);
-        s[blk] = mfma32(kop, qreg[st], s[blk]);
+        s[blk] = mfma32(kop, qreg[st], st == 0 ? (ROPE ? cneg : f32x16{}) : s[blk]);
       }
     }
   };
 
   f32x16 oacc[4];
-  float mref = -INFINITY;  // reference max (log2 units), identical in both lane halves
+  float sum0 = INFINITY;   // start of the row sums: +inf until the first reset forces it
   float lsum = 0.f;        // this lane half's partial sum of p
   auto reset_acc = [&]() __attribute__((always_inline)) {
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb) oacc[mb] = f32x16{};
     mref = -INFINITY;
+    cbase = 0.f;
+    cneg = f32x16{};
+    sum0 = INFINITY;
     lsum = 0.f;
   };
-  const float c2 = a.c2;
   const uint32_t ones = 0x3f803f80u;  // bf16 (1, 1)
 
-  // p = exp2(s c - mref) for the 32 keys of one key block as two bf16 MFMA
-  // operands (16 keys each); returns this lane's sum of p
-  auto softmax_p = [&](const f32x16& s, bf16x8 pop[2]) __attribute__((always_inline)) {
+  const float c2 = a.c2;
+  // p = exp2(s) (rotated query: scores already relative to the reference) or
+  // exp2(s c2 - mref) for the 32 keys of one key block as two bf16 MFMA
+  // operands (16 keys each); returns tsum plus this lane's sum of p
+  auto softmax_p = [&](const f32x16& s, bf16x8 pop[2], float tsum) __attribute__((always_inline)) {
     const float nm = -mref;
-    float tsum = 0.f;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       uint32_t pw[4];
 #pragma unroll
       for (int e = 0; e < 8; e += 2) {
-        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[8 * ks + e], c2, nm));
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[8 * ks + e + 1], c2, nm));
+        const float p0 = __builtin_amdgcn_exp2f(ROPE ? s[8 * ks + e] : fmaf(s[8 * ks + e], c2, nm));
+        const float p1 = __builtin_amdgcn_exp2f(ROPE ? s[8 * ks + e + 1] : fmaf(s[8 * ks + e + 1], c2, nm));
         pw[e >> 1] = pack_bf16x2(p0, p1);
         tsum = dot2(pw[e >> 1], ones, tsum);
       }
@@ -405,25 +424,37 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
     return tsum;
   };
 
-  // Probabilities of one key block.  A block whose row sum of p leaves
-  // [0, 2^64) resets the reference to the running max, rescaling the output
-  // (which may already hold the other block of the same tile, computed with
-  // the old reference) and the sum (see the header).
-  auto softmax_blk = [&](const f32x16& s, bf16x8 pop[2]) __attribute__((always_inline)) {
-    float tsum = softmax_p(s, pop);
+  // Probabilities of one key block.  The first block (its sum starts at
+  // +inf) and a block whose row sum of p leaves [0, 2^64) reset the
+  // reference to the running max, rescaling the output (which may already
+  // hold the other block of the same tile) and the sum (see the header).
+  // Score blocks already computed from the old offset are shifted to the new
+  // one (shift_pending(delta)).
+  auto softmax_blk = [&](f32x16& s, bf16x8 pop[2], auto&& shift_pending) __attribute__((always_inline)) {
+    float tsum = softmax_p(s, pop, sum0);
     if (__builtin_amdgcn_ballot_w64(!(tsum < kSumLimit)) != 0) {
+      sum0 = 0.f;
       float m = fmaxf(s[0], s[1]);
 #pragma unroll
       for (int i = 2; i < 16; ++i) m = fmaxf(m, s[i]);
-      const float mnew = fmaxf(mref, wave_half_max(m) * c2);
+      const float mnew = fmaxf(mref, ROPE ? wave_half_max(m) + cbase : wave_half_max(m) * c2);
       const float alpha = __builtin_amdgcn_exp2f(mref - mnew);
       lsum *= alpha;
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) oacc[mb][i] *= alpha;
+      if (ROPE) {
+        const float delta = mnew - cbase;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) s[i] -= delta;
+        shift_pending(delta);
+        cbase = mnew;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) cneg[i] = -mnew;
+      }
       mref = mnew;
-      tsum = softmax_p(s, pop);
+      tsum = softmax_p(s, pop, 0.f);
     }
     lsum += tsum;
   };
@@ -445,11 +476,27 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
 
   // softmax and PV of one score tile, one key block at a time, so that the
   // second block's softmax overlaps the first block's PV products
-  auto softmax_pv = [&](const f32x16 s[2], const uint16_t* vb) __attribute__((always_inline)) {
+  auto shift = [&](f32x16& x, float delta) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) x[i] -= delta;
+  };
+  // (snext: the scores of the next tile, already computed, or null)
+  auto softmax_pv = [&](f32x16 s[2], const uint16_t* vb, f32x16* snext) __attribute__((always_inline)) {
     bf16x8 pop0[2], pop1[2];
-    softmax_blk(s[0], pop0);
+    softmax_blk(s[0], pop0, [&](float delta) __attribute__((always_inline)) {
+      shift(s[1], delta);
+      if (snext) {
+        shift(snext[0], delta);
+        shift(snext[1], delta);
+      }
+    });
     pv_blk(vb, pop0, 0);
-    softmax_blk(s[1], pop1);
+    softmax_blk(s[1], pop1, [&](float delta) __attribute__((always_inline)) {
+      if (snext) {
+        shift(snext[0], delta);
+        shift(snext[1], delta);
+      }
+    });
     pv_blk(vb, pop1, 1);
   };
 
@@ -492,7 +539,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
     }
     dma_tile(vbh, j + 1, vfree, vg0, vg1);
     qk(knext, snext);
-    softmax_pv(scur, vcur);
+    softmax_pv(scur, vcur, snext);
     if (ROPE_K) store_k(kfree, kn, cs);
     __builtin_amdgcn_s_waitcnt(0);  // this wave's copies have landed
     __syncthreads();
@@ -528,7 +575,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
             if (key >= lv) s[blk][i] = -INFINITY;
           }
       }
-      softmax_pv(s, (j & 1) ? V1 : V0);
+      softmax_pv(s, (j & 1) ? V1 : V0, nullptr);
     }
   };
 
@@ -635,7 +682,10 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
   a.nqt = (Lq + BM - 1) / BM;
   const long nwg = (long)a.nqt * B * H;
   a.nwg = (int)nwg;
-  // p = exp2(c2 * (qsign q).k - m): |scale| goes into the exponent, its sign into q
+  // rotated query: scores in log2 units straight from the products,
+  // p = exp2(k . (scale log2(e) q) - m); unrotated query: p = exp2(c2 *
+  // (qsign q).k - m), |scale| in the exponent and its sign in q
+  a.qmul = scale * 1.4426950408889634f;
   a.c2 = scale == 0.f ? 1.f : fabsf(scale) * 1.4426950408889634f;
   a.qsign = scale > 0.f ? 1.f : (scale < 0.f ? -1.f : 0.f);
   a.rp = rp;

@@ -321,11 +321,12 @@ def test_empty_calls_are_noops():
 
 @pytest.mark.parametrize("scale", [0.0, -0.05, 0.7])
 def test_scale_values(scale):
-    """Zero, negative and large scales.  The kernel rounds the rotated query
-    and key to bf16 before the products (as documented); with a large scale
-    the logits are large and that input rounding dominates, so the reference
-    here is the oracle's attention over the oracle's rotated inputs rounded to
-    bf16 -- the remaining difference is the kernel's own arithmetic."""
+    """Zero, negative and large scales.  The kernel rounds the rotated key,
+    and the rotated query multiplied by scale * log2(e), to bf16 before the
+    products (as documented); with a large scale the logits are large and that
+    input rounding dominates, so the reference here is the oracle's attention
+    over the oracle's rotated inputs rounded the same way -- the remaining
+    difference is the kernel's own arithmetic."""
     import torch
 
     w = inputs.custom(f"scale{scale}", B=1, H=2, Lq=300, Lk=400, seed=28, grid=(1, 15, 20))
@@ -336,7 +337,10 @@ def test_scale_values(scale):
     ob, lse = to_bits(res[0]), res[1].cpu().numpy()
     dec = oracle.bf16_bits_to_f64
     spec = spec_of(w)
-    qr = dec(oracle.f64_to_bf16_bits(oracle.rope3d_ref(dec(q), spec)))
+    # the query's multiplier as the kernel forms it (fp32 product)
+    c = float(np.float32(np.float32(scale) * np.float32(1.4426950408889634)))
+    qrot = oracle.rope3d_ref(dec(q), spec)
+    qr = dec(oracle.f64_to_bf16_bits(qrot * c)) / c if c != 0.0 else qrot
     kr = dec(oracle.f64_to_bf16_bits(oracle.rope3d_ref(dec(k), spec)))
     ro, rl = oracle.attn_ref(qr, kr, dec(v), scale)
     assert_parity(ob, ro, f"scale {scale} vs rounded rotated inputs")
