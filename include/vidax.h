@@ -40,6 +40,7 @@
 #ifndef VIDAX_H
 #define VIDAX_H
 
+#include <stddef.h>
 #include <stdint.h>
 #include <hip/hip_runtime_api.h>
 
@@ -47,7 +48,7 @@
 extern "C" {
 #endif
 
-#define VIDAX_ABI_VERSION 7
+#define VIDAX_ABI_VERSION 8
 
 typedef enum vidax_status {
   VIDAX_OK = 0,
@@ -169,28 +170,48 @@ vidax_status vidax_attn_fwd(const void* q, const void* k, const void* v, void* o
  *   q, o, dout, dq : bf16 [B, Lq, H, d];  k, v, dk, dv : bf16 [B, Lk, H, d]
  *   lse   : fp32 [B, H, Lq], the natural-log sum-exp vidax_attn_fwd returned
  *           with the same q, k, v, scale and kv_valid_len (o is its output).
- *   delta : fp32 [B, H, Lq] device workspace owned by the caller; holds D on
- *           return.
+ *   workspace : fp32 device workspace owned by the caller, workspace_floats
+ *           values, at least B * H * Lq (VIDAX_ERR_INVALID_ARG below); its
+ *           first B * H * Lq values hold D on return (layout [B, H, Lq]).
+ *           With at least vidax_attn_bwd_workspace_floats(B, H, Lq, Lk, d)
+ *           values the key-side kernels may cut the query stream into runs
+ *           handled by separate workgroups, their partial dK and dV summed
+ *           in fp32 in the rest of the workspace (faster when
+ *           B * H * ceil(Lk / 256) is small against the compute units, e.g.
+ *           text cross-attention); with fewer they run unsplit.  Both give
+ *           the same gradients up to the order of the fp32 sums.
  *   scale, kv_valid_len: as for vidax_attn_fwd.
  * q and k are the vectors the scores were formed from: when the forward
  * rotated them, pass the rotated ones (vidax_rope3d) and take dq, dk back
  * through vidax_rope3d_transpose.  All device pointers 16-byte aligned (lse,
- * delta too); outputs must not overlap each other or any input.  Products
+ * workspace too); outputs and the workspace must not overlap each other or
+ * any input.  Products
  * run on bf16 inputs (P and ds rounded to bf16) with fp32 accumulation.
  * Requires d == 128 (VIDAX_ERR_UNSUPPORTED otherwise); B, H, Lq, Lk >= 0.
  * Buffer offsets are 32-bit and relative to a 64-row tile: 64 * H * d * 2
  * bytes must stay below 2 GiB - 4 KiB (VIDAX_ERR_UNSUPPORTED beyond).
  */
 vidax_status vidax_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout,
-                            const float* lse, void* dq, void* dk, void* dv, float* delta, int32_t B, int32_t H,
-                            int32_t Lq, int32_t Lk, int32_t d, float scale, const int32_t* kv_valid_len,
-                            hipStream_t stream);
+                            const float* lse, void* dq, void* dk, void* dv, float* workspace,
+                            size_t workspace_floats, int32_t B, int32_t H, int32_t Lq, int32_t Lk, int32_t d,
+                            float scale, const int32_t* kv_valid_len, hipStream_t stream);
+
+/*
+ * fp32 values of vidax_attn_bwd's workspace with which it splits the query
+ * stream of its key-side kernels on the current device (the split depends on
+ * the device's compute-unit count); B * H * Lq when it would not split; 0 for
+ * invalid arguments (a negative size, d != 128, a product that overflows).
+ * Makes no device call besides querying the current device's attributes.
+ */
+size_t vidax_attn_bwd_workspace_floats(int32_t B, int32_t H, int32_t Lq, int32_t Lk, int32_t d);
 
 /*
  * Allocation-free variant of vidax_attn_bwd, for callers that cannot allocate
  * device memory or pass a workspace (code under HIP graph capture, tight
  * serving loops, harnesses that forbid hipMalloc).  Same arguments, meaning,
- * layouts, results and errors as vidax_attn_bwd without `delta`: D lives in a
+ * layouts, results and errors as vidax_attn_bwd without a workspace (it runs
+ * unsplit, so its gradients equal those of vidax_attn_bwd given a workspace
+ * of exactly B * H * Lq values): D lives in a
  * fixed device array of the library (VIDAX_NOALLOC_MAX_ROWS fp32 values,
  * 16 MiB, one copy per GPU, looked up once per device on the first call with
  * that device current and held until the process ends).  The call itself

@@ -24,6 +24,7 @@ EXPORTED_SYMBOLS = (
     "vidax_rope3d",
     "vidax_rope3d_transpose",
     "vidax_attn_bwd",
+    "vidax_attn_bwd_workspace_floats",
     "vidax_attn_bwd_noalloc",
     "vidax_na3d_fwd",
     "vidax_qkv_proj",
@@ -89,8 +90,10 @@ def lib() -> ctypes.CDLL:
         L.vidax_rope3d.restype = i32
         L.vidax_rope3d_transpose.argtypes = [vp, vp, i32, i32, i32, i32, ctypes.POINTER(RopeDesc), vp]
         L.vidax_rope3d_transpose.restype = i32
-        L.vidax_attn_bwd.argtypes = [vp] * 10 + [i32, i32, i32, i32, i32, f32, vp, vp]
+        L.vidax_attn_bwd.argtypes = [vp] * 10 + [ctypes.c_size_t, i32, i32, i32, i32, i32, f32, vp, vp]
         L.vidax_attn_bwd.restype = i32
+        L.vidax_attn_bwd_workspace_floats.argtypes = [i32, i32, i32, i32, i32]
+        L.vidax_attn_bwd_workspace_floats.restype = ctypes.c_size_t
         L.vidax_attn_bwd_noalloc.argtypes = [vp] * 9 + [i32, i32, i32, i32, i32, f32, vp, vp]
         L.vidax_attn_bwd_noalloc.restype = i32
         L.vidax_na3d_fwd.argtypes = [vp] * 5 + [i32] * 10 + [f32, vp]
@@ -165,12 +168,15 @@ def rope3d_transpose(x, rope: Rope, out=None, stream=None):
     return y
 
 
-def attn_bwd(q, k, v, o, dout, lse, scale=None, kv_valid_len=None, stream=None, noalloc=False, out=None):
+def attn_bwd(q, k, v, o, dout, lse, scale=None, kv_valid_len=None, stream=None, noalloc=False, out=None,
+             workspace=None):
     """(dq, dk, dv) of attention without rotation, from the forward's o and lse.
 
     noalloc=True calls vidax_attn_bwd_noalloc (D in the library's fixed
     device array instead of a workspace tensor); `out` = (dq, dk, dv) tensors
-    to write into instead of new ones."""
+    to write into instead of new ones; `workspace` = a contiguous float32
+    device tensor to use as the workspace (by default one of
+    vidax_attn_bwd_workspace_floats values is allocated)."""
     import torch
 
     for n, t in (("q", q), ("k", k), ("v", v), ("o", o), ("dout", dout)):
@@ -201,10 +207,14 @@ def attn_bwd(q, k, v, o, dout, lse, scale=None, kv_valid_len=None, stream=None, 
                                             _ptr(dk), _ptr(dv), B, H, Lq, Lk, d, float(scale), _ptr(kv_valid_len),
                                             _stream(stream)))
         return dq, dk, dv
-    delta = torch.empty((B, H, Lq), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        n = lib().vidax_attn_bwd_workspace_floats(B, H, Lq, Lk, d)
+        workspace = torch.empty((max(n, B * H * Lq),), dtype=torch.float32, device=q.device)
+    elif workspace.dtype != torch.float32 or not workspace.is_cuda or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous float32 device tensor")
     _check("vidax_attn_bwd", lib().vidax_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(dout), _ptr(lse), _ptr(dq),
-                                                  _ptr(dk), _ptr(dv), _ptr(delta), B, H, Lq, Lk, d, float(scale),
-                                                  _ptr(kv_valid_len), _stream(stream)))
+                                                  _ptr(dk), _ptr(dv), _ptr(workspace), workspace.numel(), B, H, Lq,
+                                                  Lk, d, float(scale), _ptr(kv_valid_len), _stream(stream)))
     return dq, dk, dv
 
 

@@ -67,6 +67,12 @@ struct BwdArgs {
   float c;    // scale * log2(e)
   int ntile;  // own-row tiles (of BW rows) per (b, h) of the launched kernel
   int nwg;    // workgroups of the launched kernel
+  // key-side kernels: the query stream is cut into qsplit runs of qper
+  // 64-row tiles, one workgroup each; with qsplit > 1 each writes its fp32
+  // partial dK or dV to part ([qsplit][B][Lk][H][d], dV after dK) and the
+  // reduce kernel sums them
+  int qsplit, qper;
+  float* part;
 };
 
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
@@ -230,25 +236,52 @@ __device__ __forceinline__ void store_own(uint16_t* p, const f32x16 acc[4], floa
     }
 }
 
-// ---- D_i = <dO_i, O_i>: 16 lanes per (b, i, h) row, fp32.
+// Own row as fp32 (partial of a split run): 16-byte stores.
+__device__ __forceinline__ void store_own_f32(float* p, const f32x16 acc[4], int hi) {
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+      *reinterpret_cast<float4*>(p + mb * 32 + 8 * g + 4 * hi) =
+          make_float4(acc[mb][4 * g + 0], acc[mb][4 * g + 1], acc[mb][4 * g + 2], acc[mb][4 * g + 3]);
+}
+
+// ---- D_i = <dO_i, O_i>: 16 lanes per row, fp32.  A workgroup takes 64
+// consecutive rows i of one (b, h) (the order of D, so that 16 consecutive
+// rows' results are one contiguous store), four rows per thread in flight.
+constexpr int kDeltaRows = 4;
+constexpr int kDeltaBlock = 16 * kDeltaRows;  // rows per workgroup
 __global__ __launch_bounds__(256) void bwd_delta_kernel(BwdArgs a) {
   const int c = threadIdx.x & 15;
-  const long rows = (long)a.B * a.Lq * a.H;
-  for (long r = (long)blockIdx.x * 16 + (threadIdx.x >> 4); r < rows; r += (long)gridDim.x * 16) {
-    const uint4 x = *reinterpret_cast<const uint4*>(a.dout + r * D + c * 8);
-    const uint4 y = *reinterpret_cast<const uint4*>(a.o + r * D + c * 8);
-    const uint32_t xw[4] = {x.x, x.y, x.z, x.w}, yw[4] = {y.x, y.y, y.z, y.w};
-    float s = 0.f;
+  const int nblk = (a.Lq + kDeltaBlock - 1) / kDeltaBlock;
+  const int bh = blockIdx.x / nblk;
+  const int i0 = (blockIdx.x - bh * nblk) * kDeltaBlock + (threadIdx.x >> 4);
+  const int h = bh % a.H, b = bh / a.H;
+  const size_t tok = (size_t)a.H * D;
+  const uint16_t* dob = a.dout + (size_t)b * a.Lq * tok + (size_t)h * D + c * 8;
+  const uint16_t* ob = a.o + (size_t)b * a.Lq * tok + (size_t)h * D + c * 8;
+  uint4 x[kDeltaRows], y[kDeltaRows];
+#pragma unroll
+  for (int u = 0; u < kDeltaRows; ++u) {
+    const int i = i0 + 16 * u;
+    x[u] = y[u] = make_uint4(0, 0, 0, 0);
+    if (i < a.Lq) {
+      x[u] = *reinterpret_cast<const uint4*>(dob + (size_t)i * tok);
+      y[u] = *reinterpret_cast<const uint4*>(ob + (size_t)i * tok);
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < kDeltaRows; ++u) {
+    const uint32_t xw[4] = {x[u].x, x[u].y, x[u].z, x[u].w}, yw[4] = {y[u].x, y[u].y, y[u].z, y[u].w};
+    float sum = 0.f;
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
-      s = fmaf(bf16lo_to_f32(xw[p]), bf16lo_to_f32(yw[p]), s);
-      s = fmaf(bf16hi_to_f32(xw[p]), bf16hi_to_f32(yw[p]), s);
+      sum = fmaf(bf16lo_to_f32(xw[p]), bf16lo_to_f32(yw[p]), sum);
+      sum = fmaf(bf16hi_to_f32(xw[p]), bf16hi_to_f32(yw[p]), sum);
     }
-    s = row16_sum(s);
-    if (c == 0) {
-      const long h = r % a.H, bi = r / a.H, i = bi % a.Lq, b = bi / a.Lq;
-      a.delta[((size_t)b * a.H + h) * a.Lq + i] = s;
-    }
+    sum = row16_sum(sum);
+    const int i = i0 + 16 * u;
+    if (c == 0 && i < a.Lq) a.delta[(size_t)bh * a.Lq + i] = sum;
   }
 }
 
@@ -342,20 +375,34 @@ __global__ __launch_bounds__(NT) void bwd_kv_kernel(BwdArgs a) {
   __shared__ __attribute__((aligned(16))) float Lt[2][BN], Dt[2][BN];
   const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // logical order: key tiles innermost, so the workgroups streaming one
+  // query run of one (b, h) are neighbours (same XCD, shared L2)
   const int lid = logical_tile(blockIdx.x, a.nwg);
-  const int kt = lid % a.ntile, bh = lid / a.ntile, h = bh % a.H, b = bh / a.H;
+  const int kt = lid % a.ntile, sbh = lid / a.ntile, sp = sbh % a.qsplit, bh = sbh / a.qsplit;
+  const int h = bh % a.H, b = bh / a.H;
   const int tok = a.H * D, rbytes = tok * 2;
   const int lv = valid_keys(a, b);
   const int krow = kt * BW + wave * 32 + l32;
   const bool klive = krow < a.Lk;
   const bool kvalid = krow < lv;
+  // a wave none of whose 32 keys is valid does its share of the copies and
+  // barriers but no products
+  const bool wlive = kt * BW + wave * 32 < lv;
   const size_t rowoff = ((size_t)b * a.Lk + (klive ? krow : 0)) * tok + (size_t)h * D;
   uint16_t* outp = (DK ? a.dk : a.dv) + rowoff;
+  // fp32 partial of this run: [qsplit][B][Lk][H][d], dV's after dK's
+  float* partp =
+      a.qsplit > 1 ? a.part + ((size_t)(DK ? 0 : a.qsplit) + sp) * ((size_t)a.B * a.Lk * tok) + rowoff : nullptr;
   f32x16 acc[4];
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) acc[mb] = f32x16{};
+  auto finish = [&](float mul) __attribute__((always_inline)) {
+    if (!klive) return;
+    if (a.qsplit > 1) store_own_f32(partp, acc, hi);
+    else store_own(outp, acc, mul, hi);
+  };
   if (kt * BW >= lv) {  // no valid key in this workgroup: zero gradient
-    if (klive) store_own(outp, acc, 0.f, hi);
+    finish(0.f);
     return;
   }
   bf16x8 kop[8], vop[8];
@@ -367,9 +414,16 @@ __global__ __launch_bounds__(NT) void bwd_kv_kernel(BwdArgs a) {
   const float* lseb = a.lse + ((size_t)b * a.H + h) * a.Lq;
   const float* delb = a.delta + ((size_t)b * a.H + h) * a.Lq;
   const Staging sg = staging(wave, lane, rbytes);
-  const int ntiles = (a.Lq + BN - 1) / BN;
-  // copies and per-row lse, D of query tile t (rows past Lq: P = 0)
-  auto copies = [&](int t, uint16_t* qk, uint16_t* tv, uint16_t* ok, int buf) __attribute__((always_inline)) {
+  // this workgroup's run of query tiles [t0, t1)
+  const int t0 = sp * a.qper;
+  const int t1 = min(t0 + a.qper, (a.Lq + BN - 1) / BN);
+  // copies of query tile t, and its per-row lse and D into registers (rows
+  // past Lq: P = 0); put_rows stores those into LDS.  The stores come at the
+  // end of a step, where the step waits for its copies anyway: a wave's
+  // vector memory operations complete in issue order, so an LDS store right
+  // after the loads would make the wave wait for the tile copies too.
+  float lrow = INFINITY, drow = 0.f;
+  auto copies = [&](int t, uint16_t* qk, uint16_t* tv, uint16_t* ok) __attribute__((always_inline)) {
     const __amdgpu_buffer_rsrc_t rq = tile_rsrc(qbh, t, a.Lq, tok);
     const __amdgpu_buffer_rsrc_t ro = tile_rsrc(obh, t, a.Lq, tok);
     copy_rows(rq, qk, sg);
@@ -381,19 +435,31 @@ __global__ __launch_bounds__(NT) void bwd_kv_kernel(BwdArgs a) {
     }
     if (tid < BN) {
       const int r = t * BN + tid;
-      Lt[buf][tid] = r < a.Lq ? lseb[r] * kLog2e : INFINITY;
-      if (DK) Dt[buf][tid] = r < a.Lq ? delb[r] : 0.f;
+      lrow = r < a.Lq ? lseb[r] : INFINITY;
+      if (DK) drow = r < a.Lq ? delb[r] : 0.f;
     }
   };
-  copies(0, Qk0, Tv0, Ok0, 0);
+  auto put_rows = [&](int buf) __attribute__((always_inline)) {
+    if (tid < BN) {
+      Lt[buf][tid] = lrow * kLog2e;
+      if (DK) Dt[buf][tid] = drow;
+    }
+  };
+  if (t0 >= t1) {  // empty run
+    finish(0.f);
+    return;
+  }
+  copies(t0, Qk0, Tv0, Ok0);
+  put_rows(0);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
   auto step = [&](auto par, int t) __attribute__((always_inline)) {
     constexpr int P = decltype(par)::value;
-    if (t + 1 < ntiles) copies(t + 1, P ? Qk0 : Qk1, P ? Tv0 : Tv1, P ? Ok0 : Ok1, 1 - P);
+    if (t + 1 < t1) copies(t + 1, P ? Qk0 : Qk1, P ? Tv0 : Tv1, P ? Ok0 : Ok1);
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
+      if (!wlive) break;
       f32x16 s = rows_x_own(P ? Qk1 : Qk0, kop, blk, lane);
       f32x16 dp;
       if (DK) dp = rows_x_own(P ? Ok1 : Ok0, vop, blk, lane);
@@ -418,37 +484,85 @@ __global__ __launch_bounds__(NT) void bwd_kv_kernel(BwdArgs a) {
       pack_ops(s, op);
       tr_x_op(P ? Tv1 : Tv0, op, blk, acc, lane);
     }
+    if (t + 1 < t1) put_rows(1 - P);
     __builtin_amdgcn_s_waitcnt(0);  // this wave's copies have landed
     __syncthreads();
   };
   using even = std::integral_constant<int, 0>;
   using odd = std::integral_constant<int, 1>;
-  int t = 0;
-  for (; t + 1 < ntiles; t += 2) {
+  int t = t0;
+  for (; t + 1 < t1; t += 2) {
     step(even(), t);
     step(odd(), t + 1);
   }
-  if (t < ntiles) step(even(), t);
-  if (klive) store_own(outp, acc, DK ? a.scale : 1.f, hi);
+  if (t < t1) step(even(), t);
+  finish(DK ? a.scale : 1.f);
+}
+
+// ---- dK = scale * sum of the partials, dV = sum of the partials (qsplit >
+// 1): 8 consecutive d values of one (b, key, h) row per thread.
+__global__ __launch_bounds__(256) void bwd_reduce_kernel(BwdArgs a) {
+  const size_t n = (size_t)a.B * a.Lk * a.H * D;  // elements per gradient
+  const size_t groups = n / 8;
+  for (size_t g = (size_t)blockIdx.x * 256 + threadIdx.x; g < 2 * groups; g += (size_t)gridDim.x * 256) {
+    const bool isk = g < groups;
+    const size_t e = (isk ? g : g - groups) * 8;
+    const float* src = a.part + (isk ? 0 : (size_t)a.qsplit * n) + e;
+    float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
+    for (int sp = 0; sp < a.qsplit; ++sp) {
+      const float4 u = *reinterpret_cast<const float4*>(src + (size_t)sp * n);
+      const float4 v = *reinterpret_cast<const float4*>(src + (size_t)sp * n + 4);
+      x0.x += u.x; x0.y += u.y; x0.z += u.z; x0.w += u.w;
+      x1.x += v.x; x1.y += v.y; x1.z += v.z; x1.w += v.w;
+    }
+    const float mul = isk ? a.scale : 1.f;
+    uint4 o;
+    o.x = pack_bf16x2(x0.x * mul, x0.y * mul);
+    o.y = pack_bf16x2(x0.z * mul, x0.w * mul);
+    o.z = pack_bf16x2(x1.x * mul, x1.y * mul);
+    o.w = pack_bf16x2(x1.z * mul, x1.w * mul);
+    *reinterpret_cast<uint4*>((isk ? a.dk : a.dv) + e) = o;
+  }
 }
 
 }  // namespace
 
+// Compute units of the current device (queried once per device).
+int device_cu_count() {
+  static std::mutex mu;
+  static int counts[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  std::lock_guard<std::mutex> lock(mu);
+  if (counts[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    counts[dev] = n;
+  }
+  return counts[dev];
+}
+
 hipError_t launch_attn_bwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, const uint16_t* o,
-                           const uint16_t* dout, const float* lse, float* delta, uint16_t* dq, uint16_t* dk,
-                           uint16_t* dv, int B, int H, int Lq, int Lk, float scale, const int32_t* kv_valid_len,
-                           hipStream_t stream) {
+                           const uint16_t* dout, const float* lse, float* ws, size_t ws_floats, uint16_t* dq,
+                           uint16_t* dk, uint16_t* dv, int B, int H, int Lq, int Lk, float scale,
+                           const int32_t* kv_valid_len, hipStream_t stream) {
   BwdArgs a;
-  a.q = q; a.k = k; a.v = v; a.o = o; a.dout = dout; a.lse = lse; a.delta = delta;
+  a.q = q; a.k = k; a.v = v; a.o = o; a.dout = dout; a.lse = lse; a.delta = ws;
   a.dq = dq; a.dk = dk; a.dv = dv; a.kv_valid_len = kv_valid_len;
   a.B = B; a.H = H; a.Lq = Lq; a.Lk = Lk;
   a.scale = scale;
   a.c = scale * kLog2e;
+  BwdSplit sp = attn_bwd_split(B, H, Lq, Lk, device_cu_count());
+  if (ws_floats < sp.floats) {  // too small a workspace for the split: run unsplit
+    sp.qsplit = 1;
+    sp.qper = (Lq + BN - 1) / BN;
+  }
+  a.qsplit = sp.qsplit;
+  a.qper = sp.qper;
+  a.part = sp.qsplit > 1 ? ws + sp.part_offset : nullptr;
   hipError_t e = hipSuccess;
   if (Lq > 0) {
-    const long rows = (long)B * Lq * H;
-    long g = (rows + 15) / 16;
-    if (g > 4096) g = 4096;
+    const long g = (long)B * H * ((Lq + kDeltaBlock - 1) / kDeltaBlock);
     e = launch_kernel(bwd_delta_kernel, (unsigned)g, 256u, stream, a);
     if (e != hipSuccess) return e;
     a.ntile = (Lq + BW - 1) / BW;
@@ -458,10 +572,17 @@ hipError_t launch_attn_bwd(const uint16_t* q, const uint16_t* k, const uint16_t*
   }
   if (Lk > 0) {
     a.ntile = (Lk + BW - 1) / BW;
-    a.nwg = a.ntile * B * H;
+    a.nwg = a.ntile * B * H * a.qsplit;
     e = launch_kernel(bwd_kv_kernel<false>, (unsigned)a.nwg, (unsigned)NT, stream, a);
     if (e != hipSuccess) return e;
     e = launch_kernel(bwd_kv_kernel<true>, (unsigned)a.nwg, (unsigned)NT, stream, a);
+    if (e != hipSuccess) return e;
+    if (a.qsplit > 1) {
+      const size_t groups = 2 * (size_t)B * Lk * H * D / 8;
+      size_t g = (groups + 255) / 256;
+      if (g > 16384) g = 16384;
+      e = launch_kernel(bwd_reduce_kernel, (unsigned)g, 256u, stream, a);
+    }
   }
   return e;
 }
@@ -508,7 +629,9 @@ hipError_t launch_attn_bwd_noalloc(const uint16_t* q, const uint16_t* k, const u
   float* delta = nullptr;
   const hipError_t e = scratch_address(&delta);
   if (e != hipSuccess) return e;
-  return launch_attn_bwd(q, k, v, o, dout, lse, delta, dq, dk, dv, B, H, Lq, Lk, scale, kv_valid_len, stream);
+  // D only (the array holds no room for split partials): unsplit
+  return launch_attn_bwd(q, k, v, o, dout, lse, delta, (size_t)B * H * Lq, dq, dk, dv, B, H, Lq, Lk, scale,
+                         kv_valid_len, stream);
 }
 
 }  // namespace vidax

@@ -146,30 +146,33 @@ vidax_status rope3d_common(bool inverse, const void* x, void* y, int32_t B, int3
 }
 
 // The backward's checks; `noalloc`: D goes to the library's fixed device
-// array (delta is ignored and must be NULL) instead of the caller's workspace.
+// array (the workspace must be NULL, of 0 values) instead of the caller's.
 vidax_status bwd_common(bool noalloc, const void* q, const void* k, const void* v, const void* o, const void* dout,
-                        const float* lse, void* dq, void* dk, void* dv, float* delta, int32_t B, int32_t H,
-                        int32_t Lq, int32_t Lk, int32_t d, float scale, const int32_t* kv_valid_len,
+                        const float* lse, void* dq, void* dk, void* dv, float* ws, size_t ws_floats, int32_t B,
+                        int32_t H, int32_t Lq, int32_t Lk, int32_t d, float scale, const int32_t* kv_valid_len,
                         hipStream_t stream) {
   if (B < 0 || H < 0 || Lq < 0 || Lk < 0 || d < 0) return VIDAX_ERR_INVALID_ARG;
   const int64_t nq = numel4(B, Lq, H, d), nk = numel4(B, Lk, H, d);
   if (nq < 0 || nk < 0) return VIDAX_ERR_INVALID_ARG;
-  const int64_t nrow = (int64_t)B * H * Lq;  // lse, delta
+  const int64_t nrow = (int64_t)B * H * Lq;  // lse, D
   if ((nq > 0 && (!q || !o || !dout || !dq)) || (nk > 0 && (!k || !v || !dk || !dv)) ||
-      (nrow > 0 && (!lse || (!noalloc && !delta))))
+      (nrow > 0 && (!lse || (!noalloc && !ws))))
     return VIDAX_ERR_INVALID_ARG;
-  if (noalloc && delta) return VIDAX_ERR_INVALID_ARG;
+  if (noalloc && (ws || ws_floats)) return VIDAX_ERR_INVALID_ARG;
+  if (!noalloc && (uint64_t)ws_floats < (uint64_t)nrow) return VIDAX_ERR_INVALID_ARG;
+  if (ws_floats > ((uint64_t)1 << 60)) return VIDAX_ERR_INVALID_ARG;
+  if (!ws) ws_floats = 0;
   for (const void* p : {q, k, v, o, dout, (const void*)dq, (const void*)dk, (const void*)dv})
     if (!aligned(p, 16)) return VIDAX_ERR_INVALID_ARG;
-  if (!aligned(lse, 16) || !aligned(delta, 16)) return VIDAX_ERR_INVALID_ARG;
+  if (!aligned(lse, 16) || !aligned(ws, 16)) return VIDAX_ERR_INVALID_ARG;
   if (kv_valid_len && !aligned(kv_valid_len, 4)) return VIDAX_ERR_INVALID_ARG;
   if (!isfinite(scale)) return VIDAX_ERR_INVALID_ARG;
   if (d != vidax::kHeadDim) return VIDAX_ERR_UNSUPPORTED;
   const uint64_t qb = (uint64_t)nq * 2, kb = (uint64_t)nk * 2, rb = (uint64_t)nrow * 4;
   const uint64_t vb = kv_valid_len ? (uint64_t)B * 4 : 0;
-  // outputs (dq, dk, dv, delta) must not overlap each other or any input
-  const void* outs[4] = {dq, dk, dv, delta};
-  const uint64_t osz[4] = {qb, kb, kb, delta ? rb : 0};
+  // outputs (dq, dk, dv, the workspace) must not overlap each other or any input
+  const void* outs[4] = {dq, dk, dv, ws};
+  const uint64_t osz[4] = {qb, kb, kb, (uint64_t)ws_floats * 4};
   const void* ins[7] = {q, k, v, o, dout, lse, kv_valid_len};
   const uint64_t isz[7] = {qb, kb, kb, qb, qb, rb, vb};
   for (int i = 0; i < 4; ++i) {
@@ -178,8 +181,10 @@ vidax_status bwd_common(bool noalloc, const void* q, const void* k, const void* 
     for (int j = i + 1; j < 4; ++j)
       if (overlaps(outs[i], osz[i], outs[j], osz[j])) return VIDAX_ERR_INVALID_ARG;
   }
-  const int64_t grid = ((int64_t)(Lq > Lk ? Lq : Lk) + 255) / 256 * B * H;
-  if (grid > INT32_MAX) return VIDAX_ERR_UNSUPPORTED;
+  // grids: D pass ceil(Lq / 64) B H, dq ceil(Lq / 256) B H, key side up to
+  // 16 ceil(Lk / 256) B H
+  const int64_t grid_q = ((int64_t)Lq + 63) / 64 * B * H, grid_k = ((int64_t)Lk + 255) / 256 * 16 * B * H;
+  if (grid_q > INT32_MAX || grid_k > INT32_MAX) return VIDAX_ERR_UNSUPPORTED;
   // buffer offsets are 32-bit and relative to a 64-row tile
   if ((int64_t)64 * H * d * 2 > INT32_MAX - 4096) return VIDAX_ERR_UNSUPPORTED;
   if (noalloc && nrow > vidax::kNoAllocRows) return VIDAX_ERR_TOO_LARGE;
@@ -189,8 +194,8 @@ vidax_status bwd_common(bool noalloc, const void* q, const void* k, const void* 
                                                (const uint16_t*)o, (const uint16_t*)dout, lse, (uint16_t*)dq,
                                                (uint16_t*)dk, (uint16_t*)dv, B, H, Lq, Lk, scale, kv_valid_len, stream)
               : vidax::launch_attn_bwd((const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)o,
-                                       (const uint16_t*)dout, lse, delta, (uint16_t*)dq, (uint16_t*)dk, (uint16_t*)dv,
-                                       B, H, Lq, Lk, scale, kv_valid_len, stream);
+                                       (const uint16_t*)dout, lse, ws, ws_floats, (uint16_t*)dq, (uint16_t*)dk,
+                                       (uint16_t*)dv, B, H, Lq, Lk, scale, kv_valid_len, stream);
   return e == hipSuccess ? VIDAX_OK : VIDAX_ERR_LAUNCH;
 }
 
@@ -199,17 +204,25 @@ vidax_status bwd_common(bool noalloc, const void* q, const void* k, const void* 
 extern "C" {
 
 vidax_status vidax_attn_bwd(const void* q, const void* k, const void* v, const void* o, const void* dout,
-                            const float* lse, void* dq, void* dk, void* dv, float* delta, int32_t B, int32_t H,
-                            int32_t Lq, int32_t Lk, int32_t d, float scale, const int32_t* kv_valid_len,
-                            hipStream_t stream) {
-  return bwd_common(false, q, k, v, o, dout, lse, dq, dk, dv, delta, B, H, Lq, Lk, d, scale, kv_valid_len, stream);
+                            const float* lse, void* dq, void* dk, void* dv, float* workspace,
+                            size_t workspace_floats, int32_t B, int32_t H, int32_t Lq, int32_t Lk, int32_t d,
+                            float scale, const int32_t* kv_valid_len, hipStream_t stream) {
+  return bwd_common(false, q, k, v, o, dout, lse, dq, dk, dv, workspace, workspace_floats, B, H, Lq, Lk, d, scale,
+                    kv_valid_len, stream);
+}
+
+size_t vidax_attn_bwd_workspace_floats(int32_t B, int32_t H, int32_t Lq, int32_t Lk, int32_t d) {
+  if (B < 0 || H < 0 || Lq < 0 || Lk < 0 || d != vidax::kHeadDim) return 0;
+  if (numel4(B, Lq, H, d) < 0 || numel4(B, Lk, H, d) < 0) return 0;
+  return vidax::attn_bwd_split(B, H, Lq, Lk, vidax::device_cu_count()).floats;
 }
 
 vidax_status vidax_attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* o, const void* dout,
                                     const float* lse, void* dq, void* dk, void* dv, int32_t B, int32_t H,
                                     int32_t Lq, int32_t Lk, int32_t d, float scale, const int32_t* kv_valid_len,
                                     hipStream_t stream) {
-  return bwd_common(true, q, k, v, o, dout, lse, dq, dk, dv, nullptr, B, H, Lq, Lk, d, scale, kv_valid_len, stream);
+  return bwd_common(true, q, k, v, o, dout, lse, dq, dk, dv, nullptr, 0, B, H, Lq, Lk, d, scale, kv_valid_len,
+                    stream);
 }
 
 vidax_status vidax_qk_norm_rope(const void* x, void* y, const float* gain, float eps, int32_t B, int32_t L, int32_t H,

@@ -12,10 +12,11 @@ hipError_t launch_rope3d(const uint16_t*, uint16_t*, int, int, int, const RopePa
   return no_launch();
 }
 hipError_t launch_attn_bwd(const uint16_t*, const uint16_t*, const uint16_t*, const uint16_t*, const uint16_t*,
-                           const float*, float*, uint16_t*, uint16_t*, uint16_t*, int, int, int, int, float,
+                           const float*, float*, size_t, uint16_t*, uint16_t*, uint16_t*, int, int, int, int, float,
                            const int32_t*, hipStream_t) {
   return no_launch();
 }
+int device_cu_count() { return 256; }
 hipError_t launch_attn_bwd_noalloc(const uint16_t*, const uint16_t*, const uint16_t*, const uint16_t*,
                                    const uint16_t*, const float*, uint16_t*, uint16_t*, uint16_t*, int, int, int,
                                    int, float, const int32_t*, hipStream_t) {

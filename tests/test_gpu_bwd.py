@@ -116,6 +116,10 @@ BWD = [
     inputs.custom("bwd_one", B=2, H=1, Lq=1, Lk=1, seed=35),
     inputs.custom("bwd_edges", B=1, H=2, Lq=257, Lk=65, seed=36),
     inputs.custom("bwd_normed", B=1, H=2, Lq=1536, Lk=1536, seed=37, rms_norm_qk=True),
+    # few key workgroups and a long query stream: the key-side kernels cut the
+    # 127 query tiles into 15 runs of 9 (fp32 partials summed afterwards), the
+    # last run one tile; a batch with few valid keys
+    inputs.custom("bwd_split", B=2, H=4, Lq=8100, Lk=300, seed=38, kv_valid=("fixed", [300, 45])),
 ]
 
 
@@ -147,6 +151,40 @@ def test_attn_bwd_random_shapes(w):
 @pytest.mark.parametrize("scale", [0.0, -0.05, 0.3])
 def test_attn_bwd_scale_values(scale):
     _bwd_case(inputs.custom("bwd_scale", B=1, H=2, Lq=300, Lk=200, seed=38), scale=scale)
+
+
+def test_attn_bwd_split_matches_unsplit():
+    """The same call with a workspace that holds only D (no query-stream
+    split) and with the size vidax_attn_bwd_workspace_floats asks for (split
+    into runs): dq identical, dk and dv equal up to the order of the fp32 sums:
+    one bf16 ulp of the larger magnitude, plus 2^-12 of the (batch, head)
+    slice's RMS where a sum cancels to near zero (the summation-order error
+    scales with the summands, not with the result); zeros exactly zero."""
+    import torch
+
+    w = [c for c in BWD if c.name == "bwd_split"][0]
+    q, k, v, lv = inputs.make_qkv(w)
+    do = inputs.make_dout(w)
+    log(f"case split vs unsplit {w.name}")
+    dev = [to_dev(x) for x in (q, k, v, do)]
+    lvd = lengths_dev(lv)
+    o, lse = vx.attn_fwd(dev[0], dev[1], dev[2], scale=w.scale, kv_valid_len=lvd, return_lse=True)
+    n_split = vx.lib().vidax_attn_bwd_workspace_floats(w.B, w.H, w.Lq, w.Lk, w.d)
+    rows = w.B * w.H * w.Lq
+    assert n_split > rows  # this shape splits
+    full = vx.attn_bwd(dev[0], dev[1], dev[2], o, dev[3], lse, scale=w.scale, kv_valid_len=lvd)
+    ws = torch.empty((rows,), dtype=torch.float32, device="cuda")
+    one = vx.attn_bwd(dev[0], dev[1], dev[2], o, dev[3], lse, scale=w.scale, kv_valid_len=lvd, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(full[0].view(torch.int16), one[0].view(torch.int16)), "dq"
+    for name, a, b in zip(("dk", "dv"), full[1:], one[1:]):
+        a, b = a.float(), b.float()
+        assert bool(torch.isfinite(a).all()), name
+        rms = torch.sqrt((a * a).mean(dim=(1, 3), keepdim=True))  # per (b, h)
+        tol = 2.0 ** -7 * torch.maximum(a.abs(), b.abs()) + 2.0 ** -12 * rms
+        excess = ((a - b).abs() - tol).max()
+        assert bool(excess <= 0), (name, float((a - b).abs().max()), float(excess))
+        assert bool(((a == 0) == (b == 0)).all()), name
 
 
 def test_attn_bwd_empty_calls():

@@ -25,7 +25,7 @@ def test_library_exports_every_declared_function():
     assert set(declared) == set(vx.EXPORTED_SYMBOLS), declared
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.vidax_abi_version() == 7
+    assert lib.vidax_abi_version() == 8
     for s, text in [(0, b"ok"), (1, b"invalid argument"), (2, b"unsupported configuration"), (3, b"kernel launch failed")]:
         assert lib.vidax_status_string(s) == text
     assert b"allocation-free" in lib.vidax_status_string(4)
@@ -135,12 +135,13 @@ def _bwd_call(noalloc=False):
     f = vx.lib().vidax_attn_bwd_noalloc if noalloc else vx.lib().vidax_attn_bwd
 
     def call(q=P, k=2 * P, v=3 * P, o=4 * P, do=5 * P, lse=6 * P, dq=7 * P, dk=8 * P, dv=9 * P, delta=10 * P,
-             B=1, H=2, Lq=64, Lk=64, d=128, scale=0.088, kv=None):
+             B=1, H=2, Lq=64, Lk=64, d=128, scale=0.088, kv=None, ws_floats=None):
         ptr = lambda x: ctypes.c_void_p(x) if x else None
         if noalloc:
             return f(ptr(q), ptr(k), ptr(v), ptr(o), ptr(do), ptr(lse), ptr(dq), ptr(dk), ptr(dv),
                      B, H, Lq, Lk, d, scale, ptr(kv), None)
-        return f(ptr(q), ptr(k), ptr(v), ptr(o), ptr(do), ptr(lse), ptr(dq), ptr(dk), ptr(dv), ptr(delta),
+        n = max(B * H * Lq, 0) if ws_floats is None else ws_floats
+        return f(ptr(q), ptr(k), ptr(v), ptr(o), ptr(do), ptr(lse), ptr(dq), ptr(dk), ptr(dv), ptr(delta), n,
                  B, H, Lq, Lk, d, scale, ptr(kv), None)
     return call
 
@@ -165,6 +166,27 @@ def test_attn_bwd_rejects_invalid_arguments():
     assert call(delta=6 * P) == INV           # workspace aliases lse
     assert call(kv=7 * P + 32) == INV         # lengths overlap dq
     assert call(kv=10 * P) == INV             # lengths alias the workspace
+    assert call(ws_floats=2 * 64 - 1) == INV  # workspace smaller than D
+    assert call(ws_floats=P // 4, kv=10 * P + P // 2) == INV  # a larger workspace reaching the lengths
+    assert call(ws_floats=P // 4, dv=10 * P + 4096) == INV     # ... or an output
+    assert call(ws_floats=2 ** 62) == INV     # absurd size
+
+
+def test_attn_bwd_workspace_floats():
+    f = vx.lib().vidax_attn_bwd_workspace_floats
+    assert f(-1, 2, 64, 64, 128) == 0
+    assert f(1, 2, 64, 64, 96) == 0
+    assert f(1, 2, 0, 64, 128) == 0
+    # many key workgroups, or too few query tiles to cut: D only
+    assert f(1, 12, 32760, 32760, 128) == 12 * 32760
+    assert f(1, 2, 512, 512, 128) == 2 * 512
+    # text cross-attention shape: 2 x 40 x ceil(512 / 256) = 160 key workgroups
+    # -> cut into runs; D (padded to 64 values) then 2 x qsplit partial tensors
+    n = f(2, 40, 32760, 512, 128)
+    rows = 2 * 40 * 32760
+    grad = 2 * 512 * 40 * 128
+    assert n > rows and (n - (rows + 63) // 64 * 64) % (2 * grad) == 0
+    assert 2 <= (n - (rows + 63) // 64 * 64) // (2 * grad) <= 16
 
 
 def test_attn_bwd_noalloc_rejects_invalid_arguments():

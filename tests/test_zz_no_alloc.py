@@ -1,8 +1,9 @@
 """The allocation-free backward (vidax_attn_bwd_noalloc) against the backward
 with a caller workspace (vidax_attn_bwd), through the C ABI.
 
-Both run the same kernels; only where D is kept differs, so the gradients
-must agree bit for bit.  Two calls in a row share the library's device array:
+Both run the same kernels when the workspace holds exactly D (B * H * Lq
+values: no query-stream split); only where D is kept differs, so the
+gradients must agree bit for bit.  Two calls in a row share the library's device array:
 the first at the array's maximum size (B * H * Lq = VIDAX_NOALLOC_MAX_ROWS),
 the second smaller, so a second call that read stale values of the first
 would differ.  A request one row beyond the maximum is rejected with
@@ -45,14 +46,15 @@ def test_noalloc_matches_workspace_backward_twice():
     for c in cases:
         log(f"noalloc backward B={c['B']} H={c['H']} Lq={c['Lq']} Lk={c['Lk']} lens={c['lens']}")
         q, k, v, o, do, lse, lv = _case(torch, c["B"], c["H"], c["Lq"], c["Lk"], c["lens"], c["seed"])
-        ref = vx.attn_bwd(q, k, v, o, do, lse, kv_valid_len=lv)
+        ws = torch.empty((c["B"] * c["H"] * c["Lq"],), dtype=torch.float32, device="cuda")
+        ref = vx.attn_bwd(q, k, v, o, do, lse, kv_valid_len=lv, workspace=ws)
         out = tuple(torch.full_like(t, float("nan")) for t in ref)  # stale contents must be overwritten
         got = vx.attn_bwd(q, k, v, o, do, lse, kv_valid_len=lv, noalloc=True, out=out)
         torch.cuda.synchronize()
         for name, a, b in zip(("dq", "dk", "dv"), got, ref):
             assert _same_bits(torch, a, b), name
             assert bool(torch.isfinite(a.float()).all()), name
-        del q, k, v, o, do, lse, ref, got, out
+        del q, k, v, o, do, lse, ref, got, out, ws
         torch.cuda.empty_cache()
 
 
