@@ -187,6 +187,53 @@ def test_attn_bwd_split_matches_unsplit():
         assert bool(((a == 0) == (b == 0)).all()), name
 
 
+def test_attn_bwd_batch_over_2gib():
+    """One batch of k, v (and dk, dv) larger than 2 GiB: B=1, H=40, Lk=220000
+    keys, 64 queries.  Element (n, h) of k sits at byte (n * 40 + h) * 256,
+    past 2 GiB from key row 209716 on; the kernels rebase each 64-row tile
+    with 64-bit pointers and keep 32-bit offsets inside it.  Checked against
+    the oracle's exact gradient: dq of every query and dk, dv of key rows on
+    both sides of the 2 GiB offset and at the end, for the first and last
+    head (the largest offsets).  Inputs are seeded N(0, 1) drawn on the GPU
+    (torch's generator) and copied back for the heads the oracle checks; the
+    forward takes batches below 2 GiB only, so o and lse come from plain fp32
+    attention on the GPU."""
+    import torch
+
+    B, H, Lq, Lk = 1, 40, 64, 220000
+    g = torch.Generator(device="cuda")
+    g.manual_seed(39)
+    mk = lambda L: torch.randn((B, L, H, 128), generator=g, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    q, k, v, do = mk(Lq), mk(Lk), mk(Lk), mk(Lq)
+    assert k.numel() * 2 > 2 ** 31
+    scale = float(np.float32(1 / np.sqrt(128)))
+    log(f"case bwd over 2 GiB B{B} H{H} Lq{Lq} Lk{Lk}")
+    # the forward takes batches below 2 GiB only: o and lse here are plain
+    # fp32 softmax attention, one head at a time (an input of the backward;
+    # the expected gradients come from the oracle alone)
+    o = torch.empty_like(q)
+    lse = torch.empty((B, H, Lq), dtype=torch.float32, device="cuda")
+    for h in range(H):
+        sc = (q[0, :, h].float() @ k[0, :, h].float().T) * scale
+        lse[0, h] = torch.logsumexp(sc, dim=1)
+        o[0, :, h] = (torch.softmax(sc, dim=1) @ v[0, :, h].float()).to(torch.bfloat16)
+    del sc
+    dq, dk, dv = vx.attn_bwd(q, k, v, o, do, lse, scale=scale)
+    torch.cuda.synchronize()
+    hs = [0, H - 1]
+    krows = np.array([0, 1, 4097, 100000, 209663, 209715, 209716, 209790, 215000, 219935, 219998, 219999])
+    bits = lambda t: t[:, :, hs].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    dec = oracle.bf16_bits_to_f64
+    qh, kh, vh, doh = (dec(bits(t)) for t in (q, k, v, do))
+    got_dq = bits(dq)
+    got_dk = dk[:, torch.from_numpy(krows).cuda()][:, :, hs].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    got_dv = dv[:, torch.from_numpy(krows).cuda()][:, :, hs].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    rq, rk, rv = oracle.attn_bwd_ref_rows(qh, kh, vh, doh, scale, np.arange(Lq), krows, workers=16)
+    _check_grad(got_dq, rq, "dq, heads 0 and 39")
+    _check_grad(got_dk, rk, "dk rows across 2 GiB")
+    _check_grad(got_dv, rv, "dv rows across 2 GiB")
+
+
 def test_attn_bwd_empty_calls():
     import torch
 
