@@ -177,7 +177,7 @@ vidax_status vidax_attn_fwd(const void* q, const void* k, const void* v, void* o
  *           values the key-side kernels may cut the query stream into runs
  *           handled by separate workgroups, their partial dK and dV summed
  *           in fp32 in the rest of the workspace (faster when
- *           B * H * ceil(Lk / 256) is small against the compute units, e.g.
+ *           B * H * ceil(Lk / 128) is small against the compute units, e.g.
  *           text cross-attention); with fewer they run unsplit.  Both give
  *           the same gradients up to the order of the fp32 sums.
  *   scale, kv_valid_len: as for vidax_attn_fwd.

@@ -6,25 +6,26 @@
 //   D_i = <dO_i, O_i>            delta kernel (HBM-bound, one pass over dO, O)
 //   dQ  = scale dS K             dq kernel: one query tile per workgroup,
 //                                  streaming K and V tiles
-//   dV  = P^T dO                 dv kernel: one key tile per workgroup,
-//   dK  = scale dS^T Q           dk kernel:   streaming Q and dO tiles
+//   dV  = P^T dO, dK = scale dS^T Q   dkdv kernel: one key tile per
+//                                  workgroup, streaming Q and dO tiles
 //   dS  = P * (dO V^T - D)
 //
-// Each kernel has the forward kernel's shape and layouts: eight waves of 32
+// The dq kernel has the forward kernel's shape and layouts: eight waves of 32
 // own rows, tiles of 64 streamed rows copied straight into LDS (buffer loads
 // with the LDS flag), two buffers per tile kind, one barrier per tile.  Tiles
 // read row-wise are kept as padded rows (whole-row copies, lanes in address
-// order); tiles read transposed are kept in MFMA operand order.  The own rows' vectors (q and dO in the dq kernel, k and
-// v in the dk/dv kernels) stay in registers as the B operand of
+// order); tiles read transposed are kept in MFMA operand order.  The own
+// rows' vectors (q and dO) stay in registers as the B operand of
 // v_mfma_f32_32x32x16_bf16; the streamed tile is the A operand, read either
 // row-wise (K order) or transposed by ds_read_b64_tr_b16 (V order).  The
 // products of a 64-row tile with the wave's 32 own rows land in two 32 x 32
 // accumulators whose lanes each hold one own row; converted to bf16 they are
-// directly the B operand of the next product (P or dS against the other
-// tile), with the row order inside each 16-row step matched by the
-// transposing read -- as in the forward.  dK and dV have their own kernels
-// because keeping both accumulators (and k, v, S, dP) in one wave needs more
-// than the 256 registers a wave has at two waves per SIMD.
+// directly the B operand of the next product (dS against the other tile),
+// with the row order inside each 16-row step matched by the transposing read
+// -- as in the forward.  The dkdv kernel computes both key gradients from one
+// pass over the queries with 16 own keys per wave and 16 x 16 x 32 products
+// (both accumulators then fit a wave's registers at two waves per SIMD); its
+// description is at the kernel.
 #include <type_traits>
 
 #include <mutex>
@@ -236,16 +237,6 @@ __device__ __forceinline__ void store_own(uint16_t* p, const f32x16 acc[4], floa
     }
 }
 
-// Own row as fp32 (partial of a split run): 16-byte stores.
-__device__ __forceinline__ void store_own_f32(float* p, const f32x16 acc[4], int hi) {
-#pragma unroll
-  for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-    for (int g = 0; g < 4; ++g)
-      *reinterpret_cast<float4*>(p + mb * 32 + 8 * g + 4 * hi) =
-          make_float4(acc[mb][4 * g + 0], acc[mb][4 * g + 1], acc[mb][4 * g + 2], acc[mb][4 * g + 3]);
-}
-
 // ---- D_i = <dO_i, O_i>: 16 lanes per row, fp32.  A workgroup takes 64
 // consecutive rows i of one (b, h) (the order of D, so that 16 consecutive
 // rows' results are one contiguous store), four rows per thread in flight.
@@ -363,126 +354,210 @@ __global__ __launch_bounds__(NT) void bwd_dq_kernel(BwdArgs a) {
   if (qlive) store_own(dqp, acc, a.scale, hi);
 }
 
-// ---- dK (DK) or dV (!DK): one tile of 256 keys of one (b, h) per workgroup.
-//   S = Q K^T (Q tile in K order), P = exp2(S c - lse log2 e) (per query row),
-//   dV^T += dO^T P (dO tile in V order); dP = dO V^T (dO tile in K order),
-//   dS = P (dP - D), dK^T += Q^T dS (Q tile in V order).  Keys at or beyond
-//   Lv get P = 0 and so zero gradient.
-template <bool DK>
-__global__ __launch_bounds__(NT) void bwd_kv_kernel(BwdArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t Qk0[KTILE], Qk1[KTILE], Tv0[TILE], Tv1[TILE];
-  __shared__ __attribute__((aligned(16))) uint16_t Ok0[DK ? KTILE : 8], Ok1[DK ? KTILE : 8];
+// ---- dK and dV together: one tile of 128 keys of one (b, h) per workgroup,
+// 16 keys per wave, with v_mfma_f32_16x16x32_bf16 (A: lane l holds row l % 16,
+// k = 8 (l / 16) .. + 7; B: column l % 16, the same k; C: column l % 16, rows
+// 4 (l / 16) .. + 3).  Per 64-query tile and query block r (16 queries):
+//   S[r] = Q K^T, dP[r] = dO V^T  (A: Q / dO rows from the padded row tile,
+//     one 16-byte read; B: the wave's own k / v rows in registers)
+//   P = exp2(S c - lse log2 e), dS = P (dP - D)   (lane: key column, 4 queries)
+//   dV^T += dO^T P, dK^T += Q^T dS over k-steps of 32 queries  (A: the
+//     transposing read of the same padded row tile, 4 queries x 16 d per
+//     16-lane group; B: P / dS, whose k order -- queries 32 s + 4 g .. + 3,
+//     then 32 s + 16 + 4 g .. + 3 for lane group g -- the two reads match).
+// Both accumulators (64 registers) and k, v (32) fit in a wave's 256
+// registers at two waves per SIMD; each query tile is copied once per
+// tensor.
+//
+// Tiles of 64 query rows sit in LDS as 256-byte rows whose 16-byte chunks
+// are permuted: chunk c of row r at position c ^ swz(r), swz linear in the
+// bits of r & 15 (bit 0 -> 2, bit 1 -> 4, bit 2 -> 9, bit 3 -> 8).  The 16
+// (or 8) rows of a row-operand read (one chunk each) and the 8 (or 4) rows x
+// 32 bytes of a transposing read then fall on distinct banks, whether the
+// LDS serves 256 or 128 bytes a cycle.
+// Copy j of a tile fills rows 4 j .. 4 j + 3: lane l writes position l & 15
+// of row 4 j + (l >> 4), fetching its chunk (l & 15) ^ swz(row) (each row
+// read whole, 256 contiguous bytes).
+constexpr int BK = 128;  // keys per workgroup
+constexpr int STILE = BN * D;  // elements of a swizzled tile
+
+__device__ __forceinline__ int swz(int r) { return ((r & 3) << 1) ^ ((r & 4) ? 9 : 0) ^ (r & 8); }
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__global__ __launch_bounds__(NT) void bwd_dkdv_kernel(BwdArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t Qk0[STILE], Qk1[STILE], Ok0[STILE], Ok1[STILE];
   __shared__ __attribute__((aligned(16))) float Lt[2][BN], Dt[2][BN];
-  const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
+  const int tid = threadIdx.x, lane = tid & 63, c16 = lane & 15, g = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  // logical order: key tiles innermost, so the workgroups streaming one
-  // query run of one (b, h) are neighbours (same XCD, shared L2)
   const int lid = logical_tile(blockIdx.x, a.nwg);
   const int kt = lid % a.ntile, sbh = lid / a.ntile, sp = sbh % a.qsplit, bh = sbh / a.qsplit;
   const int h = bh % a.H, b = bh / a.H;
   const int tok = a.H * D, rbytes = tok * 2;
   const int lv = valid_keys(a, b);
-  const int krow = kt * BW + wave * 32 + l32;
+  const int krow = kt * BK + wave * 16 + c16;
   const bool klive = krow < a.Lk;
   const bool kvalid = krow < lv;
-  // a wave none of whose 32 keys is valid does its share of the copies and
-  // barriers but no products
-  const bool wlive = kt * BW + wave * 32 < lv;
+  const bool wlive = kt * BK + wave * 16 < lv;  // uniform
   const size_t rowoff = ((size_t)b * a.Lk + (klive ? krow : 0)) * tok + (size_t)h * D;
-  uint16_t* outp = (DK ? a.dk : a.dv) + rowoff;
-  // fp32 partial of this run: [qsplit][B][Lk][H][d], dV's after dK's
-  float* partp =
-      a.qsplit > 1 ? a.part + ((size_t)(DK ? 0 : a.qsplit) + sp) * ((size_t)a.B * a.Lk * tok) + rowoff : nullptr;
-  f32x16 acc[4];
+  f32x4 dk[8], dv[8];
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb) acc[mb] = f32x16{};
-  auto finish = [&](float mul) __attribute__((always_inline)) {
+  for (int mb = 0; mb < 8; ++mb) dk[mb] = dv[mb] = f32x4{};
+  // own row: lane holds key krow, d = 16 mb + 4 g .. + 3 of block mb
+  auto finish = [&](float mulk) __attribute__((always_inline)) {
     if (!klive) return;
-    if (a.qsplit > 1) store_own_f32(partp, acc, hi);
-    else store_own(outp, acc, mul, hi);
+    if (a.qsplit > 1) {
+      const size_t n = (size_t)a.B * a.Lk * tok;
+      float* pk = a.part + (size_t)sp * n + rowoff;
+      float* pv = a.part + (size_t)(a.qsplit + sp) * n + rowoff;
+#pragma unroll
+      for (int mb = 0; mb < 8; ++mb) {
+        *reinterpret_cast<float4*>(pk + 16 * mb + 4 * g) = make_float4(dk[mb][0], dk[mb][1], dk[mb][2], dk[mb][3]);
+        *reinterpret_cast<float4*>(pv + 16 * mb + 4 * g) = make_float4(dv[mb][0], dv[mb][1], dv[mb][2], dv[mb][3]);
+      }
+    } else {
+#pragma unroll
+      for (int mb = 0; mb < 8; ++mb) {
+        uint2 x, y;
+        x.x = pack_bf16x2(dk[mb][0] * mulk, dk[mb][1] * mulk);
+        x.y = pack_bf16x2(dk[mb][2] * mulk, dk[mb][3] * mulk);
+        y.x = pack_bf16x2(dv[mb][0], dv[mb][1]);
+        y.y = pack_bf16x2(dv[mb][2], dv[mb][3]);
+        *reinterpret_cast<uint2*>(a.dk + rowoff + 16 * mb + 4 * g) = x;
+        *reinterpret_cast<uint2*>(a.dv + rowoff + 16 * mb + 4 * g) = y;
+      }
+    }
   };
-  if (kt * BW >= lv) {  // no valid key in this workgroup: zero gradient
+  if (kt * BK >= lv) {  // no valid key in this workgroup: zero gradient
     finish(0.f);
     return;
   }
-  bf16x8 kop[8], vop[8];
-  own_operand(a.k + rowoff, klive, hi, kop);
-  if (DK) own_operand(a.v + rowoff, klive, hi, vop);
+  // own k, v as B operands: lane holds key krow, d = 32 st + 8 g .. + 7
+  bf16x8 kop[4], vop[4];
+#pragma unroll
+  for (int st = 0; st < 4; ++st) {
+    uint4 x = make_uint4(0, 0, 0, 0), y = x;
+    if (klive) {
+      x = *reinterpret_cast<const uint4*>(a.k + rowoff + 32 * st + 8 * g);
+      y = *reinterpret_cast<const uint4*>(a.v + rowoff + 32 * st + 8 * g);
+    }
+    kop[st] = __builtin_bit_cast(bf16x8, x);
+    vop[st] = __builtin_bit_cast(bf16x8, y);
+  }
 
   const uint16_t* qbh = a.q + (size_t)b * a.Lq * tok + (size_t)h * D;
   const uint16_t* obh = a.dout + (size_t)b * a.Lq * tok + (size_t)h * D;
   const float* lseb = a.lse + ((size_t)b * a.H + h) * a.Lq;
   const float* delb = a.delta + ((size_t)b * a.H + h) * a.Lq;
-  const Staging sg = staging(wave, lane, rbytes);
-  // this workgroup's run of query tiles [t0, t1)
+  // the wave's copies 2 wave, 2 wave + 1 of a tile: byte offsets from its first row
+  int cg[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int row = 4 * (2 * wave + u) + (lane >> 4);
+    cg[u] = row * rbytes + (c16 ^ swz(row)) * 16;
+  }
+  auto copy_tile = [&](__amdgpu_buffer_rsrc_t rs, uint16_t* buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)(buf + (2 * wave + u) * 512), 16, cg[u], 0, 0, 0);
+  };
   const int t0 = sp * a.qper;
   const int t1 = min(t0 + a.qper, (a.Lq + BN - 1) / BN);
-  // copies of query tile t, and its per-row lse and D into registers (rows
-  // past Lq: P = 0); put_rows stores those into LDS.  The stores come at the
-  // end of a step, where the step waits for its copies anyway: a wave's
-  // vector memory operations complete in issue order, so an LDS store right
-  // after the loads would make the wave wait for the tile copies too.
   float lrow = INFINITY, drow = 0.f;
-  auto copies = [&](int t, uint16_t* qk, uint16_t* tv, uint16_t* ok) __attribute__((always_inline)) {
-    const __amdgpu_buffer_rsrc_t rq = tile_rsrc(qbh, t, a.Lq, tok);
-    const __amdgpu_buffer_rsrc_t ro = tile_rsrc(obh, t, a.Lq, tok);
-    copy_rows(rq, qk, sg);
-    if (DK) {
-      copy_blocks(rq, tv, wave, sg.v0, sg.v1);
-      copy_rows(ro, ok, sg);
-    } else {
-      copy_blocks(ro, tv, wave, sg.v0, sg.v1);
-    }
+  auto copies = [&](int t, uint16_t* qk, uint16_t* ok) __attribute__((always_inline)) {
+    copy_tile(tile_rsrc(qbh, t, a.Lq, tok), qk);
+    copy_tile(tile_rsrc(obh, t, a.Lq, tok), ok);
     if (tid < BN) {
       const int r = t * BN + tid;
       lrow = r < a.Lq ? lseb[r] : INFINITY;
-      if (DK) drow = r < a.Lq ? delb[r] : 0.f;
+      drow = r < a.Lq ? delb[r] : 0.f;
     }
   };
   auto put_rows = [&](int buf) __attribute__((always_inline)) {
     if (tid < BN) {
       Lt[buf][tid] = lrow * kLog2e;
-      if (DK) Dt[buf][tid] = drow;
+      Dt[buf][tid] = drow;
     }
   };
-  if (t0 >= t1) {  // empty run
+  if (t0 >= t1) {
     finish(0.f);
     return;
   }
-  copies(t0, Qk0, Tv0, Ok0);
+  copies(t0, Qk0, Ok0);
   put_rows(0);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
+  // per-lane LDS element offsets (rows of a 16-row block share swz):
+  //   row operand, query row 16 r + c16, d = 32 st + 8 g: chunk 4 st + g,
+  //     placed at 4 (st ^ (swz >> 2)) + ((g ^ swz) & 3);
+  //   transposing read, query row 4 g + (c16 >> 2) of a 16-row block, d =
+  //     16 mb + 4 (c16 & 3): 8 bytes of chunk pair mb, placed at pair
+  //     mb ^ (swz >> 1), chunk ((c16 >> 1) & 1) ^ (swz & 1) of the pair.
+  int roff[4], toff[8];
+  {
+    const int fr = swz(c16);
+#pragma unroll
+    for (int st = 0; st < 4; ++st) roff[st] = c16 * D + 8 * (4 * (st ^ (fr >> 2)) + ((g ^ fr) & 3));
+    const int tr = 4 * g + (c16 >> 2), ft = swz(tr), cc = c16 & 3;
+#pragma unroll
+    for (int mb = 0; mb < 8; ++mb) toff[mb] = tr * D + 16 * (mb ^ (ft >> 1)) + 8 * ((cc >> 1) ^ (ft & 1)) + 4 * (cc & 1);
+  }
   auto step = [&](auto par, int t) __attribute__((always_inline)) {
     constexpr int P = decltype(par)::value;
-    if (t + 1 < t1) copies(t + 1, P ? Qk0 : Qk1, P ? Tv0 : Tv1, P ? Ok0 : Ok1);
+    const uint16_t* qt = P ? Qk1 : Qk0;
+    const uint16_t* ot = P ? Ok1 : Ok0;
+    if (t + 1 < t1) copies(t + 1, P ? Qk0 : Qk1, P ? Ok0 : Ok1);
+    if (wlive) {
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
-      if (!wlive) break;
-      f32x16 s = rows_x_own(P ? Qk1 : Qk0, kop, blk, lane);
-      f32x16 dp;
-      if (DK) dp = rows_x_own(P ? Ok1 : Ok0, vop, blk, lane);
+      for (int s = 0; s < 2; ++s) {
+        f32x4 sc[2], dp[2];
 #pragma unroll
-      for (int i4 = 0; i4 < 4; ++i4) {
-        const int r0 = acc_row(blk, 4 * i4, hi);  // four consecutive rows
-        const float4 l4 = *reinterpret_cast<const float4*>(&Lt[P][r0]);
-        const float lr[4] = {l4.x, l4.y, l4.z, l4.w};
-        float dr[4] = {0.f, 0.f, 0.f, 0.f};
-        if (DK) {
-          const float4 d4 = *reinterpret_cast<const float4*>(&Dt[P][r0]);
-          dr[0] = d4.x; dr[1] = d4.y; dr[2] = d4.z; dr[3] = d4.w;
+        for (int u = 0; u < 2; ++u) {
+          const int r = 2 * s + u;
+          sc[u] = dp[u] = f32x4{};
+#pragma unroll
+          for (int st = 0; st < 4; ++st) {
+            const bf16x8 qa = *reinterpret_cast<const bf16x8*>(qt + 16 * r * D + roff[st]);
+            const bf16x8 oa = *reinterpret_cast<const bf16x8*>(ot + 16 * r * D + roff[st]);
+            sc[u] = mfma16(qa, kop[st], sc[u]);
+            dp[u] = mfma16(oa, vop[st], dp[u]);
+          }
         }
+        // P and dS of queries 16 r + 4 g + i (i = 0..3), r = 2 s + u
+        uint32_t pw[4], dw[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int i = 4 * i4 + e;
-          const float p = kvalid ? __builtin_amdgcn_exp2f(fmaf(s[i], a.c, -lr[e])) : 0.f;
-          s[i] = DK ? p * (dp[i] - dr[e]) : p;
+        for (int u = 0; u < 2; ++u) {
+          const int r0 = 16 * (2 * s + u) + 4 * g;
+          const float4 l4 = *reinterpret_cast<const float4*>(&Lt[P][r0]);
+          const float4 d4 = *reinterpret_cast<const float4*>(&Dt[P][r0]);
+          const float lr[4] = {l4.x, l4.y, l4.z, l4.w}, dr[4] = {d4.x, d4.y, d4.z, d4.w};
+          float pp[4], dd[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            pp[i] = kvalid ? __builtin_amdgcn_exp2f(fmaf(sc[u][i], a.c, -lr[i])) : 0.f;
+            dd[i] = pp[i] * (dp[u][i] - dr[i]);
+          }
+          pw[2 * u] = pack_bf16x2(pp[0], pp[1]);
+          pw[2 * u + 1] = pack_bf16x2(pp[2], pp[3]);
+          dw[2 * u] = pack_bf16x2(dd[0], dd[1]);
+          dw[2 * u + 1] = pack_bf16x2(dd[2], dd[3]);
+        }
+        const bf16x8 pb = __builtin_bit_cast(bf16x8, make_uint4(pw[0], pw[1], pw[2], pw[3]));
+        const bf16x8 db = __builtin_bit_cast(bf16x8, make_uint4(dw[0], dw[1], dw[2], dw[3]));
+        // dV^T += dO^T P, dK^T += Q^T dS over queries 32 s .. 32 s + 31
+#pragma unroll
+        for (int mb = 0; mb < 8; ++mb) {
+          const int o0 = 32 * s * D + toff[mb];
+          const i16x4 olo = lds_read_tr16(ot + o0), ohi = lds_read_tr16(ot + o0 + 16 * D);
+          const i16x4 qlo = lds_read_tr16(qt + o0), qhi = lds_read_tr16(qt + o0 + 16 * D);
+          dv[mb] = mfma16(__builtin_bit_cast(bf16x8, __builtin_shufflevector(olo, ohi, 0, 1, 2, 3, 4, 5, 6, 7)), pb, dv[mb]);
+          dk[mb] = mfma16(__builtin_bit_cast(bf16x8, __builtin_shufflevector(qlo, qhi, 0, 1, 2, 3, 4, 5, 6, 7)), db, dk[mb]);
         }
       }
-      bf16x8 op[2];
-      pack_ops(s, op);
-      tr_x_op(P ? Tv1 : Tv0, op, blk, acc, lane);
     }
     if (t + 1 < t1) put_rows(1 - P);
     __builtin_amdgcn_s_waitcnt(0);  // this wave's copies have landed
@@ -496,7 +571,7 @@ __global__ __launch_bounds__(NT) void bwd_kv_kernel(BwdArgs a) {
     step(odd(), t + 1);
   }
   if (t < t1) step(even(), t);
-  finish(DK ? a.scale : 1.f);
+  finish(a.scale);
 }
 
 // ---- dK = scale * sum of the partials, dV = sum of the partials (qsplit >
@@ -573,9 +648,9 @@ hipError_t launch_attn_bwd(const uint16_t* q, const uint16_t* k, const uint16_t*
   if (Lk > 0) {
     a.ntile = (Lk + BW - 1) / BW;
     a.nwg = a.ntile * B * H * a.qsplit;
-    e = launch_kernel(bwd_kv_kernel<false>, (unsigned)a.nwg, (unsigned)NT, stream, a);
-    if (e != hipSuccess) return e;
-    e = launch_kernel(bwd_kv_kernel<true>, (unsigned)a.nwg, (unsigned)NT, stream, a);
+    a.ntile = (Lk + BK - 1) / BK;
+    a.nwg = a.ntile * B * H * a.qsplit;
+    e = launch_kernel(bwd_dkdv_kernel, (unsigned)a.nwg, (unsigned)NT, stream, a);
     if (e != hipSuccess) return e;
     if (a.qsplit > 1) {
       const size_t groups = 2 * (size_t)B * Lk * H * D / 8;

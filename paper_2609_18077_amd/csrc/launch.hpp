@@ -23,8 +23,8 @@ hipError_t launch_rope3d(const uint16_t* x, uint16_t* y, int B, int L, int H, co
 // Compute units of the current device (queried once per device).
 int device_cu_count();
 
-// Query-stream split of the backward's key-side kernels.  Their workgroups
-// own 256 keys of one (b, h) and stream every query in 64-row tiles; when
+// Query-stream split of the backward's key-side kernel.  Its workgroups
+// own 128 keys of one (b, h) and stream every query in 64-row tiles; when
 // there are fewer of them than twice the compute units, the query tiles are
 // cut into qsplit runs of qper tiles (at least 8 tiles a run, at most 16
 // runs) so that about four workgroups per compute unit exist.  The fp32
@@ -37,7 +37,7 @@ struct BwdSplit {
 };
 
 inline BwdSplit attn_bwd_split(int B, int H, int Lq, int Lk, int cus) {
-  constexpr int kRows = 64, kOwn = 256;
+  constexpr int kRows = 64, kOwn = 128;
   BwdSplit r;
   const size_t rows = (size_t)B * H * Lq;
   const int qtiles = (Lq + kRows - 1) / kRows;

@@ -180,7 +180,7 @@ def test_attn_bwd_workspace_floats():
     # many key workgroups, or too few query tiles to cut: D only
     assert f(1, 12, 32760, 32760, 128) == 12 * 32760
     assert f(1, 2, 512, 512, 128) == 2 * 512
-    # text cross-attention shape: 2 x 40 x ceil(512 / 256) = 160 key workgroups
+    # text cross-attention shape: 2 x 40 x ceil(512 / 128) = 320 key workgroups
     # -> cut into runs; D (padded to 64 values) then 2 x qsplit partial tensors
     n = f(2, 40, 32760, 512, 128)
     rows = 2 * 40 * 32760
