@@ -331,10 +331,11 @@ __global__ __launch_bounds__(NT) void bwd_dq_kernel(BwdArgs a) {
       f32x16 s = rows_x_own(P ? Kk1 : Kk0, qop, blk, lane);
       const f32x16 dp = rows_x_own(P ? Vk1 : Vk0, dop, blk, lane);
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float p = __builtin_amdgcn_exp2f(fmaf(s[i], a.c, -lse2));
-        if (tail && j * BN + acc_row(blk, i, hi) >= lv) p = 0.f;
-        s[i] = p * (dp[i] - dl);
+      for (int i = 0; i < 16; ++i) s[i] = __builtin_amdgcn_exp2f(fmaf(s[i], a.c, -lse2)) * (dp[i] - dl);
+      if (tail) {  // uniform: only the last, ragged key tile; keys past Lv get dS = 0
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          if (j * BN + acc_row(blk, i, hi) >= lv) s[i] = 0.f;
       }
       bf16x8 dsop[2];
       pack_ops(s, dsop);
