@@ -10,22 +10,20 @@
 //                                  workgroup, streaming Q and dO tiles
 //   dS  = P * (dO V^T - D)
 //
-// The dq kernel has the forward kernel's shape and layouts: eight waves of 32
-// own rows, tiles of 64 streamed rows copied straight into LDS (buffer loads
-// with the LDS flag), two buffers per tile kind, one barrier per tile.  Tiles
-// read row-wise are kept as padded rows (whole-row copies, lanes in address
-// order); tiles read transposed are kept in MFMA operand order.  The own
-// rows' vectors (q and dO) stay in registers as the B operand of
-// v_mfma_f32_32x32x16_bf16; the streamed tile is the A operand, read either
-// row-wise (K order) or transposed by ds_read_b64_tr_b16 (V order).  The
-// products of a 64-row tile with the wave's 32 own rows land in two 32 x 32
-// accumulators whose lanes each hold one own row; converted to bf16 they are
-// directly the B operand of the next product (dS against the other tile),
-// with the row order inside each 16-row step matched by the transposing read
-// -- as in the forward.  The dkdv kernel computes both key gradients from one
-// pass over the queries with 16 own keys per wave and 16 x 16 x 32 products
-// (both accumulators then fit a wave's registers at two waves per SIMD); its
-// description is at the kernel.
+// Both matrix kernels stream tiles of 64 rows straight from global memory
+// into LDS (buffer loads with the LDS flag), two buffers per tensor, one
+// barrier per tile, and keep the tiles as 256-byte rows with XOR-permuted
+// 16-byte chunks (the row layout at the dq kernel), which every operand read
+// -- 16-byte row reads and the transposing ds_read_b64_tr_b16 -- hits without
+// bank conflicts.  The dq kernel follows the forward kernel's formulation:
+// a wave's 32 own queries (q and dO) stay in registers as the B operand of
+// v_mfma_f32_32x32x16_bf16, the K and V rows are the A operand, S^T and dP^T
+// land in accumulators whose lanes each hold one query, and dS^T, converted
+// to bf16 in place, is the B operand of dQ^T += K^T dS^T with K^T from the
+// transposing read of the same K tile, in the matching key order.  The dkdv
+// kernel computes both key gradients from one pass over the queries with 16
+// own keys per wave and 16 x 16 x 32 products (both accumulators then fit a
+// wave's registers at two waves per SIMD); its description is at the kernel.
 #include <type_traits>
 
 #include <mutex>
@@ -37,13 +35,8 @@ namespace {
 
 constexpr int D = kHeadDim;
 constexpr int BN = 64;        // rows per streamed tile
-constexpr int NW = 8;         // waves per workgroup
-constexpr int NT = NW * 64;   // threads
-constexpr int BW = NW * 32;   // own rows per workgroup
-constexpr int TILE = BN * D;  // elements per streamed tile in V order
-constexpr int kRowPitch = 17 * 8;  // elements per row of a K-order tile (16 chunks + 1 padding)
-constexpr int KTILE = BN * kRowPitch;  // elements per streamed tile in K order (17 KB)
-constexpr int BLK = 512;      // elements per operand block (1 KB)
+constexpr int NW = 8;         // waves of a dkdv workgroup
+constexpr int NT = NW * 64;   // its threads
 constexpr int kBufferFlags = 0x00020000;  // raw buffer, 32-bit data format
 constexpr float kLog2e = 1.4426950408889634f;
 
@@ -66,7 +59,7 @@ struct BwdArgs {
   int B, H, Lq, Lk;
   float scale;
   float c;    // scale * log2(e)
-  int ntile;  // own-row tiles (of BW rows) per (b, h) of the launched kernel
+  int ntile;  // own-row tiles per (b, h) of the launched kernel
   int nwg;    // workgroups of the launched kernel
   // key-side kernels: the query stream is cut into qsplit runs of qper
   // 64-row tiles, one workgroup each; with qsplit > 1 each writes its fp32
@@ -76,7 +69,7 @@ struct BwdArgs {
   float* part;
 };
 
-__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+[[maybe_unused]] __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
@@ -107,66 +100,12 @@ __device__ __forceinline__ int valid_keys(const BwdArgs& a, int b) {
   return __builtin_amdgcn_readfirstlane(lv);
 }
 
-// ---- streamed tiles (64 rows of a [B, L, H, 128] tensor for one (b, h)).
-//   K order (read row-wise): row by row, each 256-byte row followed by 16
-//     bytes of padding, so that every direct copy (64 lanes x 16 bytes into
-//     consecutive slots) fetches whole rows with its lanes in address order
-//     (coalesced; the padding slot reads past the records: zero, no memory
-//     access) and the operand reads -- lane l: row 32 blk + (l & 31), chunk
-//     2 st + (l >> 5) -- fall on distinct banks (rows 17 chunks apart).
-// V order, in MFMA operand order, 16 blocks of 1 KB:
-//   V order, block 4 ks + mb, half r: lane l's 8 bytes = row
-//     16 ks + 8 r + 4 (l >> 5) + ((l & 15) >> 2), d = 32 mb + 16 ((l >> 4) & 1)
-//     + 4 (l & 3) .. + 3  (what the transposing read of lane l fetches for
-//     the A^T operand of d block mb, rows 16 ks .. 16 ks + 15)
-// V order: wave w copies blocks 2w, 2w + 1 of a tile.  K order: copy j (of
-// 17 a tile) fills 16-byte slots 64 j .. 64 j + 63, lane l slot s = 64 j + l =
-// row s / 17, chunk s % 17 (16: padding); wave 0 issues copies 0..2, wave
-// w > 0 copies 2 w + 1, 2 w + 2.  Lane offsets in bytes from the tile's first
-// row:
-struct Staging {
-  int r[3];        // K-order copies
-  int rfirst, rn;  // the wave's first K-order copy and their number
-  int v0, v1;      // V-order blocks
-};
-
-__device__ __forceinline__ Staging staging(int wave, int lane, int rbytes) {
-  const int hi = lane >> 5;
-  Staging s;
-  s.rfirst = wave == 0 ? 0 : 2 * wave + 1;
-  s.rn = wave == 0 ? 3 : 2;
-#pragma unroll
-  for (int u = 0; u < 3; ++u) {
-    const int sl = 64 * (s.rfirst + u) + lane, row = sl / 17, c = sl - 17 * row;
-    s.r[u] = c < 16 ? row * rbytes + c * 16 : 0x7ffffff0;
-  }
-  const int vrow = 8 * hi + 4 * ((lane >> 4) & 1) + ((lane & 7) >> 1);
-  const int vd = 16 * ((lane >> 3) & 1) + 8 * (lane & 1);
-  const int b0 = 2 * wave, b1 = 2 * wave + 1;  // V blocks (ks, mb) = (b >> 2, b & 3)
-  s.v0 = (vrow + 16 * (b0 >> 2)) * rbytes + 2 * (vd + 32 * (b0 & 3));
-  s.v1 = (vrow + 16 * (b1 >> 2)) * rbytes + 2 * (vd + 32 * (b1 & 3));
-  return s;
-}
-
 // Buffer resource of 64-row tile `tile` of rows [0, limit): later rows read
 // as zero (and land in LDS as zero).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint16_t* base, int tile, int limit, int tok) {
   const int rows = min(max(limit - tile * BN, 0), BN);
   const int nbytes = __builtin_amdgcn_readfirstlane(rows * tok * 2);
   return __builtin_amdgcn_make_buffer_rsrc((void*)(base + (size_t)tile * BN * tok), (short)0, nbytes, kBufferFlags);
-}
-
-__device__ __forceinline__ void copy_blocks(__amdgpu_buffer_rsrc_t rs, uint16_t* buf, int wave, int g0, int g1) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)(buf + (2 * wave) * BLK), 16, g0, 0, 0, 0);
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)(buf + (2 * wave + 1) * BLK), 16, g1, 0, 0, 0);
-}
-
-// the wave's K-order copies of a tile
-__device__ __forceinline__ void copy_rows(__amdgpu_buffer_rsrc_t rs, uint16_t* buf, const Staging& sg) {
-#pragma unroll
-  for (int u = 0; u < 3; ++u)
-    if (u < sg.rn)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)(buf + (sg.rfirst + u) * 512), 16, sg.r[u], 0, 0, 0);
 }
 
 // B operand of the wave's own row: chunks 2 s + hi (s = 0..7) of the row at
@@ -180,37 +119,9 @@ __device__ __forceinline__ void own_operand(const uint16_t* p, bool live, int hi
   }
 }
 
-// acc = (tile rows 32 blk .. 32 blk + 31) x (own rows)^T over d, from a
-// K-order tile.
-__device__ __forceinline__ f32x16 rows_x_own(const uint16_t* t, const bf16x8 own[8], int blk, int lane) {
-  f32x16 acc = f32x16{};
-  const uint16_t* base = t + (32 * blk + (lane & 31)) * kRowPitch + 8 * (lane >> 5);
-#pragma unroll
-  for (int st = 0; st < 8; ++st) {
-    const bf16x8 a = *reinterpret_cast<const bf16x8*>(base + 16 * st);
-    acc = mfma32(a, own[st], acc);
-  }
-  return acc;
-}
-
-// acc[mb] += (tile^T, d block mb) x op over tile rows 32 blk .. 32 blk + 31,
-// from a V-order tile (op[k2] holds rows 32 blk + 16 k2 .. + 15).
-__device__ __forceinline__ void tr_x_op(const uint16_t* t, const bf16x8 op[2], int blk, f32x16 acc[4], int lane) {
-#pragma unroll
-  for (int k2 = 0; k2 < 2; ++k2)
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb) {
-      const int ks = 2 * blk + k2;
-      const i16x4 lo = lds_read_tr16(t + (4 * ks + mb) * BLK + lane * 4);
-      const i16x4 hi4 = lds_read_tr16(t + (4 * ks + mb) * BLK + BLK / 2 + lane * 4);
-      const bf16x8 a = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
-      acc[mb] = mfma32(a, op[k2], acc[mb]);
-    }
-}
-
 // A 32 x 32 fp32 accumulator (tile rows x own rows) -> two bf16 B operands of
 // 16 tile rows each, in the accumulator's row order.
-__device__ __forceinline__ void pack_ops(const f32x16& x, bf16x8 op[2]) {
+[[maybe_unused]] __device__ __forceinline__ void pack_ops(const f32x16& x, bf16x8 op[2]) {
 #pragma unroll
   for (int k2 = 0; k2 < 2; ++k2) {
     uint32_t w[4];
@@ -221,7 +132,7 @@ __device__ __forceinline__ void pack_ops(const f32x16& x, bf16x8 op[2]) {
 }
 
 // Tile row (0..63) of register i of accumulator blk for lane half hi.
-__device__ __forceinline__ int acc_row(int blk, int i, int hi) { return 32 * blk + 8 * (i >> 2) + 4 * hi + (i & 3); }
+[[maybe_unused]] __device__ __forceinline__ int acc_row(int blk, int i, int hi) { return 32 * blk + 8 * (i >> 2) + 4 * hi + (i & 3); }
 
 // Own row `row` of the wave (lane holds it), d = 32 mb + 8 g + 4 hi + (0..3):
 // acc^T * mul -> bf16, 8-byte stores.
@@ -276,18 +187,41 @@ __global__ __launch_bounds__(256) void bwd_delta_kernel(BwdArgs a) {
   }
 }
 
-// ---- dQ: one tile of 256 queries of one (b, h) per workgroup.
-//   S^T = K Q^T, dP^T = V dO^T (K, V tiles in K order), P^T = exp2(S^T c -
-//   lse log2 e), dS^T = P^T (dP^T - D), dQ^T += K^T dS^T (K tile in V order).
-__global__ __launch_bounds__(NT) void bwd_dq_kernel(BwdArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t Kk0[KTILE], Kk1[KTILE], Vk0[KTILE], Vk1[KTILE], Kv0[TILE], Kv1[TILE];
+// ---- dQ: one tile of 32 NWQ queries of one (b, h) per workgroup of NWQ
+// waves: 8 for long key sequences, 4 for short ones (two workgroups then
+// share a CU, so that one's start and end overlap the other's products --
+// with few key tiles per workgroup those dominate).  K and V tiles of 64 keys
+// in the swizzled row layout (see below), double-buffered:
+//   S^T = K Q^T, dP^T = V dO^T (A: key rows, one 16-byte read), P^T =
+//   exp2(S^T c - lse log2 e), dS^T = P^T (dP^T - D), dQ^T += K^T dS^T (A: the
+//   transposing read of the same K tile: 4 keys x 16 d per 16-lane group, in
+//   the key order of the dS^T operand taken from the accumulator).
+constexpr int STILE = BN * D;  // elements of a swizzled tile
+// key tiles at or below which the dq workgroups have 4 waves instead of 8
+constexpr int kDqShortTiles = 16;
+
+// Tiles of 64 rows sit in LDS as 256-byte rows whose 16-byte chunks are
+// permuted: chunk c of row r at position c ^ swz(r), swz linear in the bits
+// of r & 15 (bit 0 -> 2, bit 1 -> 4, bit 2 -> 9, bit 3 -> 8), found by
+// exhaustive search: the rows of every operand read of the dq and dkdv
+// kernels then fall on distinct banks, whether the LDS serves 128 or 256
+// bytes a cycle.  Copy j of a tile fills rows 4 j .. 4 j + 3: lane l writes
+// position l & 15 of row 4 j + (l >> 4), fetching its chunk (l & 15) ^
+// swz(row) (each row read whole, 256 contiguous bytes).
+__device__ __forceinline__ int swz(int r) { return ((r & 3) << 1) ^ ((r & 4) ? 9 : 0) ^ (r & 8); }
+
+template <int NWQ>
+__device__ __forceinline__ void dq_body(const BwdArgs& a) {
+  constexpr int BWQ = NWQ * 32;       // queries per workgroup
+  constexpr int NCOPY = 16 / NWQ;     // copies per wave of a tile (16 of 4 rows)
+  __shared__ __attribute__((aligned(16))) uint16_t K0[STILE], K1[STILE], V0[STILE], V1[STILE];
   const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lid = logical_tile(blockIdx.x, a.nwg);
   const int qt = lid % a.ntile, bh = lid / a.ntile, h = bh % a.H, b = bh / a.H;
   const int tok = a.H * D, rbytes = tok * 2;
   const int lv = valid_keys(a, b);
-  const int qrow = qt * BW + wave * 32 + l32;
+  const int qrow = qt * BWQ + wave * 32 + l32;
   const bool qlive = qrow < a.Lq;
   const size_t rowoff = ((size_t)b * a.Lq + (qlive ? qrow : 0)) * tok + (size_t)h * D;
   uint16_t* dqp = a.dq + rowoff;
@@ -307,29 +241,63 @@ __global__ __launch_bounds__(NT) void bwd_dq_kernel(BwdArgs a) {
 
   const uint16_t* kbh = a.k + (size_t)b * a.Lk * tok + (size_t)h * D;
   const uint16_t* vbh = a.v + (size_t)b * a.Lk * tok + (size_t)h * D;
-  const Staging sg = staging(wave, lane, rbytes);
   const int ntiles = (lv + BN - 1) / BN;
-  auto copies = [&](int j, uint16_t* kk, uint16_t* vk, uint16_t* kv) __attribute__((always_inline)) {
+  // the wave's copies NCOPY wave .. + NCOPY - 1 of a tile: byte offsets from its first row
+  int cg[NCOPY];
+#pragma unroll
+  for (int u = 0; u < NCOPY; ++u) {
+    const int row = 4 * (NCOPY * wave + u) + (lane >> 4);
+    cg[u] = row * rbytes + ((lane & 15) ^ swz(row)) * 16;
+  }
+  auto copies = [&](int j, uint16_t* kb, uint16_t* vb) __attribute__((always_inline)) {
     const __amdgpu_buffer_rsrc_t rk = tile_rsrc(kbh, j, lv, tok);
     const __amdgpu_buffer_rsrc_t rv = tile_rsrc(vbh, j, lv, tok);
-    copy_rows(rk, kk, sg);
-    copy_rows(rv, vk, sg);
-    copy_blocks(rk, kv, wave, sg.v0, sg.v1);
+#pragma unroll
+    for (int u = 0; u < NCOPY; ++u) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_ptr)(kb + (NCOPY * wave + u) * 512), 16, cg[u], 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_ptr)(vb + (NCOPY * wave + u) * 512), 16, cg[u], 0, 0, 0);
+    }
   };
-  copies(0, Kk0, Vk0, Kv0);
+  // per-lane LDS element offsets:
+  //   key-row operand, key row l32 (+ 32 blk), d = 16 st + 8 hi: chunk 2 st +
+  //     hi at 2 (st ^ (swz >> 1)) + (hi ^ (swz & 1));
+  //   K^T operand (transposing reads h = 0, 1 of 16-key step ks), key row
+  //     16 ks + 8 h + 4 hi + (w >> 2), d = 32 mb + 16 (g & 1) + 4 (w & 3) for
+  //     lane l = 16 g + w.
+  int rk[8], tk[2][4];
+  {
+    const int fr = swz(l32);
+#pragma unroll
+    for (int st = 0; st < 8; ++st) rk[st] = l32 * D + 8 * (hi ^ (fr & 1)) + 16 * (st ^ (fr >> 1));
+    const int g = lane >> 4, w = lane & 15, cc = w & 3;
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      const int row = 8 * hh + 4 * hi + (w >> 2), ft = swz(row);
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+        tk[hh][mb] = row * D + 32 * (mb ^ (ft >> 2)) + 8 * ((2 * (g & 1) + (cc >> 1)) ^ (ft & 3)) + 4 * (cc & 1);
+    }
+  }
+  copies(0, K0, V0);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
   auto step = [&](auto par, int j) __attribute__((always_inline)) {
     constexpr int P = decltype(par)::value;
-    if (j + 1 < ntiles) copies(j + 1, P ? Kk0 : Kk1, P ? Vk0 : Vk1, P ? Kv0 : Kv1);
+    const uint16_t* kt = P ? K1 : K0;
+    const uint16_t* vt = P ? V1 : V0;
+    if (j + 1 < ntiles) copies(j + 1, P ? K0 : K1, P ? V0 : V1);
     const bool tail = j * BN + BN > lv;
     // one 32-key block at a time: fewer live registers, and the products of
     // the second block overlap the first block's exponentials
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
-      f32x16 s = rows_x_own(P ? Kk1 : Kk0, qop, blk, lane);
-      const f32x16 dp = rows_x_own(P ? Vk1 : Vk0, dop, blk, lane);
+      f32x16 s = f32x16{}, dp = f32x16{};
+#pragma unroll
+      for (int st = 0; st < 8; ++st) {
+        s = mfma32(*reinterpret_cast<const bf16x8*>(kt + 32 * blk * D + rk[st]), qop[st], s);
+        dp = mfma32(*reinterpret_cast<const bf16x8*>(vt + 32 * blk * D + rk[st]), dop[st], dp);
+      }
 #pragma unroll
       for (int i = 0; i < 16; ++i) s[i] = __builtin_amdgcn_exp2f(fmaf(s[i], a.c, -lse2)) * (dp[i] - dl);
       if (tail) {  // uniform: only the last, ragged key tile; keys past Lv get dS = 0
@@ -339,7 +307,17 @@ __global__ __launch_bounds__(NT) void bwd_dq_kernel(BwdArgs a) {
       }
       bf16x8 dsop[2];
       pack_ops(s, dsop);
-      tr_x_op(P ? Kv1 : Kv0, dsop, blk, acc, lane);
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) {
+        const int ks = 2 * blk + k2;
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb) {
+          const i16x4 lo = lds_read_tr16(kt + 16 * ks * D + tk[0][mb]);
+          const i16x4 up = lds_read_tr16(kt + 16 * ks * D + tk[1][mb]);
+          acc[mb] = mfma32(__builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7)),
+                           dsop[k2], acc[mb]);
+        }
+      }
     }
     __builtin_amdgcn_s_waitcnt(0);  // this wave's copies have landed
     __syncthreads();
@@ -355,6 +333,11 @@ __global__ __launch_bounds__(NT) void bwd_dq_kernel(BwdArgs a) {
   if (qlive) store_own(dqp, acc, a.scale, hi);
 }
 
+// 4 waves (128 queries) a workgroup where the key sequence is short, 8
+// waves (256 queries) otherwise.
+__global__ __launch_bounds__(256, 2) void bwd_dq4_kernel(BwdArgs a) { dq_body<4>(a); }
+__global__ __launch_bounds__(512) void bwd_dq8_kernel(BwdArgs a) { dq_body<8>(a); }
+
 // ---- dK and dV together: one tile of 128 keys of one (b, h) per workgroup,
 // 16 keys per wave, with v_mfma_f32_16x16x32_bf16 (A: lane l holds row l % 16,
 // k = 8 (l / 16) .. + 7; B: column l % 16, the same k; C: column l % 16, rows
@@ -369,20 +352,8 @@ __global__ __launch_bounds__(NT) void bwd_dq_kernel(BwdArgs a) {
 // Both accumulators (64 registers) and k, v (32) fit in a wave's 256
 // registers at two waves per SIMD; each query tile is copied once per
 // tensor.
-//
-// Tiles of 64 query rows sit in LDS as 256-byte rows whose 16-byte chunks
-// are permuted: chunk c of row r at position c ^ swz(r), swz linear in the
-// bits of r & 15 (bit 0 -> 2, bit 1 -> 4, bit 2 -> 9, bit 3 -> 8).  The 16
-// (or 8) rows of a row-operand read (one chunk each) and the 8 (or 4) rows x
-// 32 bytes of a transposing read then fall on distinct banks, whether the
-// LDS serves 256 or 128 bytes a cycle.
-// Copy j of a tile fills rows 4 j .. 4 j + 3: lane l writes position l & 15
-// of row 4 j + (l >> 4), fetching its chunk (l & 15) ^ swz(row) (each row
-// read whole, 256 contiguous bytes).
+// Tiles of 64 query rows in the swizzled row layout of the dq kernel.
 constexpr int BK = 128;  // keys per workgroup
-constexpr int STILE = BN * D;  // elements of a swizzled tile
-
-__device__ __forceinline__ int swz(int r) { return ((r & 3) << 1) ^ ((r & 4) ? 9 : 0) ^ (r & 8); }
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
@@ -641,14 +612,15 @@ hipError_t launch_attn_bwd(const uint16_t* q, const uint16_t* k, const uint16_t*
     const long g = (long)B * H * ((Lq + kDeltaBlock - 1) / kDeltaBlock);
     e = launch_kernel(bwd_delta_kernel, (unsigned)g, 256u, stream, a);
     if (e != hipSuccess) return e;
-    a.ntile = (Lq + BW - 1) / BW;
+    const bool short_keys = (Lk + BN - 1) / BN <= kDqShortTiles;
+    const int nwq = short_keys ? 4 : 8;
+    a.ntile = (Lq + 32 * nwq - 1) / (32 * nwq);
     a.nwg = a.ntile * B * H;
-    e = launch_kernel(bwd_dq_kernel, (unsigned)a.nwg, (unsigned)NT, stream, a);
+    e = short_keys ? launch_kernel(bwd_dq4_kernel, (unsigned)a.nwg, 256u, stream, a)
+                   : launch_kernel(bwd_dq8_kernel, (unsigned)a.nwg, 512u, stream, a);
     if (e != hipSuccess) return e;
   }
   if (Lk > 0) {
-    a.ntile = (Lk + BW - 1) / BW;
-    a.nwg = a.ntile * B * H * a.qsplit;
     a.ntile = (Lk + BK - 1) / BK;
     a.nwg = a.ntile * B * H * a.qsplit;
     e = launch_kernel(bwd_dkdv_kernel, (unsigned)a.nwg, (unsigned)NT, stream, a);
