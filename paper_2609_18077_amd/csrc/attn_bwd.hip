@@ -3,7 +3,8 @@
 // output O and natural-log sum-exp.  bf16 in/out, fp32 accumulation, head
 // dim 128.  With P = exp(scale q k^T - lse):
 //
-//   D_i = <dO_i, O_i>            delta kernel (HBM-bound, one pass over dO, O)
+//   D_i = <dO_i, O_i>            dq kernel, from the own rows' dO (loaded
+//                                  anyway) and O; written for the dkdv kernel
 //   dQ  = scale dS K             dq kernel: one query tile per workgroup,
 //                                  streaming K and V tiles
 //   dV  = P^T dO, dK = scale dS^T Q   dkdv kernel: one key tile per
@@ -77,13 +78,10 @@ __device__ __forceinline__ i16x4 lds_read_tr16(const uint16_t* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p));
 }
 
-// Sum over the 16 lanes of a row (row rotations, then quad permutations).
-__device__ __forceinline__ float row16_sum(float v) {
-  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x128, 0xf, 0xf, false));
-  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x124, 0xf, 0xf, false));
-  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4e, 0xf, 0xf, false));
-  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xb1, 0xf, 0xf, false));
-  return v;
+// Sum over lanes l and l ^ 32.
+__device__ __forceinline__ float half_sum(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 // Workgroups are dispatched round-robin over the 8 XCDs: give each XCD a
@@ -148,45 +146,6 @@ __device__ __forceinline__ void store_own(uint16_t* p, const f32x16 acc[4], floa
     }
 }
 
-// ---- D_i = <dO_i, O_i>: 16 lanes per row, fp32.  A workgroup takes 64
-// consecutive rows i of one (b, h) (the order of D, so that 16 consecutive
-// rows' results are one contiguous store), four rows per thread in flight.
-constexpr int kDeltaRows = 4;
-constexpr int kDeltaBlock = 16 * kDeltaRows;  // rows per workgroup
-__global__ __launch_bounds__(256) void bwd_delta_kernel(BwdArgs a) {
-  const int c = threadIdx.x & 15;
-  const int nblk = (a.Lq + kDeltaBlock - 1) / kDeltaBlock;
-  const int bh = blockIdx.x / nblk;
-  const int i0 = (blockIdx.x - bh * nblk) * kDeltaBlock + (threadIdx.x >> 4);
-  const int h = bh % a.H, b = bh / a.H;
-  const size_t tok = (size_t)a.H * D;
-  const uint16_t* dob = a.dout + (size_t)b * a.Lq * tok + (size_t)h * D + c * 8;
-  const uint16_t* ob = a.o + (size_t)b * a.Lq * tok + (size_t)h * D + c * 8;
-  uint4 x[kDeltaRows], y[kDeltaRows];
-#pragma unroll
-  for (int u = 0; u < kDeltaRows; ++u) {
-    const int i = i0 + 16 * u;
-    x[u] = y[u] = make_uint4(0, 0, 0, 0);
-    if (i < a.Lq) {
-      x[u] = *reinterpret_cast<const uint4*>(dob + (size_t)i * tok);
-      y[u] = *reinterpret_cast<const uint4*>(ob + (size_t)i * tok);
-    }
-  }
-#pragma unroll
-  for (int u = 0; u < kDeltaRows; ++u) {
-    const uint32_t xw[4] = {x[u].x, x[u].y, x[u].z, x[u].w}, yw[4] = {y[u].x, y[u].y, y[u].z, y[u].w};
-    float sum = 0.f;
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      sum = fmaf(bf16lo_to_f32(xw[p]), bf16lo_to_f32(yw[p]), sum);
-      sum = fmaf(bf16hi_to_f32(xw[p]), bf16hi_to_f32(yw[p]), sum);
-    }
-    sum = row16_sum(sum);
-    const int i = i0 + 16 * u;
-    if (c == 0 && i < a.Lq) a.delta[(size_t)bh * a.Lq + i] = sum;
-  }
-}
-
 // ---- dQ: one tile of 32 NWQ queries of one (b, h) per workgroup of NWQ
 // waves: 8 for long key sequences, 4 for short ones (two workgroups then
 // share a CU, so that one's start and end overlap the other's products --
@@ -225,6 +184,29 @@ __device__ __forceinline__ void dq_body(const BwdArgs& a) {
   const bool qlive = qrow < a.Lq;
   const size_t rowoff = ((size_t)b * a.Lq + (qlive ? qrow : 0)) * tok + (size_t)h * D;
   uint16_t* dqp = a.dq + rowoff;
+  const size_t lrow = ((size_t)b * a.H + h) * a.Lq + (qlive ? qrow : 0);
+  bf16x8 dop[8];
+  own_operand(a.dout + rowoff, qlive, hi, dop);
+  // D of the own row: this lane half's 64 products <dO, O>, then the other
+  // half's; stored for the dkdv kernel (every row, also without valid keys)
+  float dl;
+  {
+    bf16x8 oop[8];
+    own_operand(a.o + rowoff, qlive, hi, oop);
+    float sum = 0.f;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      const uint4 x = __builtin_bit_cast(uint4, dop[s]), y = __builtin_bit_cast(uint4, oop[s]);
+      const uint32_t xw[4] = {x.x, x.y, x.z, x.w}, yw[4] = {y.x, y.y, y.z, y.w};
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        sum = fmaf(bf16lo_to_f32(xw[p]), bf16lo_to_f32(yw[p]), sum);
+        sum = fmaf(bf16hi_to_f32(xw[p]), bf16hi_to_f32(yw[p]), sum);
+      }
+    }
+    dl = half_sum(sum);
+    if (qlive && hi == 0) a.delta[lrow] = dl;
+  }
   f32x16 acc[4];
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) acc[mb] = f32x16{};
@@ -232,12 +214,9 @@ __device__ __forceinline__ void dq_body(const BwdArgs& a) {
     if (qlive) store_own(dqp, acc, 0.f, hi);
     return;
   }
-  bf16x8 qop[8], dop[8];
+  bf16x8 qop[8];
   own_operand(a.q + rowoff, qlive, hi, qop);
-  own_operand(a.dout + rowoff, qlive, hi, dop);
-  const size_t lrow = ((size_t)b * a.H + h) * a.Lq + (qlive ? qrow : 0);
   const float lse2 = qlive ? a.lse[lrow] * kLog2e : INFINITY;  // dead rows: P = 0
-  const float dl = qlive ? a.delta[lrow] : 0.f;
 
   const uint16_t* kbh = a.k + (size_t)b * a.Lk * tok + (size_t)h * D;
   const uint16_t* vbh = a.v + (size_t)b * a.Lk * tok + (size_t)h * D;
@@ -609,9 +588,6 @@ hipError_t launch_attn_bwd(const uint16_t* q, const uint16_t* k, const uint16_t*
   a.part = sp.qsplit > 1 ? ws + sp.part_offset : nullptr;
   hipError_t e = hipSuccess;
   if (Lq > 0) {
-    const long g = (long)B * H * ((Lq + kDeltaBlock - 1) / kDeltaBlock);
-    e = launch_kernel(bwd_delta_kernel, (unsigned)g, 256u, stream, a);
-    if (e != hipSuccess) return e;
     const bool short_keys = (Lk + BN - 1) / BN <= kDqShortTiles;
     const int nwq = short_keys ? 4 : 8;
     a.ntile = (Lq + 32 * nwq - 1) / (32 * nwq);
@@ -642,8 +618,9 @@ hipError_t launch_attn_bwd(const uint16_t* q, const uint16_t* k, const uint16_t*
 // library runs on, held until the process ends.  In host code `scratch` is
 // only a stand-in for the symbol; its device address (different on every
 // GPU) is looked up once per device and only that address is handed to the
-// kernels.  Calls that overlap on one GPU share the array and race; the
-// delta kernel rewrites every value a call reads, so nothing is cleared.
+// kernels.  Calls that overlap on one GPU share the array and race; the dq
+// kernel writes every value the dkdv kernel then reads, so nothing is
+// cleared.
 static __device__ __align__(256) float scratch[kNoAllocRows];
 
 constexpr int kMaxDevices = 64;

@@ -181,9 +181,8 @@ vidax_status bwd_common(bool noalloc, const void* q, const void* k, const void* 
     for (int j = i + 1; j < 4; ++j)
       if (overlaps(outs[i], osz[i], outs[j], osz[j])) return VIDAX_ERR_INVALID_ARG;
   }
-  // grids: D pass ceil(Lq / 64) B H, dq ceil(Lq / 256) B H, key side up to
-  // 16 ceil(Lk / 128) B H
-  const int64_t grid_q = ((int64_t)Lq + 63) / 64 * B * H, grid_k = ((int64_t)Lk + 127) / 128 * 16 * B * H;
+  // grids: dq up to ceil(Lq / 128) B H, key side up to 16 ceil(Lk / 128) B H
+  const int64_t grid_q = ((int64_t)Lq + 127) / 128 * B * H, grid_k = ((int64_t)Lk + 127) / 128 * 16 * B * H;
   if (grid_q > INT32_MAX || grid_k > INT32_MAX) return VIDAX_ERR_UNSUPPORTED;
   // buffer offsets are 32-bit and relative to a 64-row tile
   if ((int64_t)64 * H * d * 2 > INT32_MAX - 4096) return VIDAX_ERR_UNSUPPORTED;
