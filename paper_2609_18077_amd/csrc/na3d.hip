@@ -5,15 +5,18 @@
 // moved inward at the border), with a softmax over that key set.  bf16 in/out,
 // fp32 accumulation, head dim 128.
 //
-// A workgroup of 8 waves owns a 2 x 8 x 16 block of queries (t, h, w); wave
-// (i, j) owns the 2 x 4 x 4 sub-block at h offset 4 i, w offset 4 j, 32
-// queries.  The union of the workgroup's windows is a box of rows (t', h')
-// times at most 26 consecutive w.  The workgroup streams that box two rows at
-// a time: each step copies the two rows' keys and values (32 w positions
-// each, from an even start) straight from global memory into LDS, double
-// buffered, one barrier per step.  A wave whose own key box contains either
-// row computes one 32-key score block from them -- 16 keys of each row, at
-// the wave's own offset along w -- as in the dense forward kernel:
+// A workgroup of 4 waves owns a 2 x 4 x 16 block of queries (t, h, w); wave
+// j owns the 2 x 4 x 4 sub-block at w offset 4 j, 32 queries, so every row
+// of the workgroup's key box lies in every wave's windows along t and h (with
+// 8 waves over a 2 x 8 x 16 block, each wave sat out the steps of the rows
+// outside its own h range, a fifth of them).  The union of the workgroup's
+// windows is a box of rows (t', h') times at most 26 consecutive w.  The
+// workgroup streams that box two rows at a time: each step copies the two
+// rows' keys and values (32 w positions each, from an even start) straight
+// from global memory into LDS, double buffered, one barrier per step; two
+// workgroups (64 KB of LDS each) share a CU.  Each wave computes one 32-key
+// score block per step -- 16 keys of each row, at its own offset along w --
+// as in the dense forward kernel:
 //
 //   S^T [32 keys x 32 queries] = K Q^T     8 x v_mfma_f32_32x32x16_bf16
 //   P^T = exp2(S^T c - m), zero outside each query's window
@@ -35,7 +38,7 @@ namespace {
 
 constexpr int D = kHeadDim;
 constexpr int QT = 2, QH = 4, QW = 4;  // query block of one wave
-constexpr int WH = 2, WW = 4;          // waves of a workgroup along h and w
+constexpr int WH = 1, WW = 4;          // waves of a workgroup along h and w
 constexpr int NW = WH * WW, NT = NW * 64;
 constexpr int ROWK = 32;               // staged keys per row
 constexpr int STEPK = 2 * ROWK;        // keys per step (two rows)
@@ -102,7 +105,7 @@ __device__ __forceinline__ int chunk_slot(int x, int c) {
   return c ^ (((m & 3) << 2) | (m >> 2));
 }
 
-__global__ __launch_bounds__(NT) void na3d_fwd_kernel(NaArgs a) {
+__global__ __launch_bounds__(NT, 2) void na3d_fwd_kernel(NaArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t K0[BUF], K1[BUF], V0[BUF], V1[BUF];
   const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hi = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -178,15 +181,15 @@ __global__ __launch_bounds__(NT) void na3d_fwd_kernel(NaArgs a) {
   // block (keys 0 .. 31 from the step's first row, 32 .. 63 from its second,
   // at w positions A0 .. A0 + 31; a missing second row repeats the first);
   // lane i fills slot i & 15 of key 4 blk + (i >> 4)
-  const int skey0 = 8 * wave + (lane >> 4);  // block 2 w; block 2 w + 1 is key + 4
+  const int skey0 = 16 * wave + (lane >> 4);  // block 4 w; block 4 w + u is key + 4 u
   auto stage = [&](int stp, int2 rowA, uint16_t* kb, uint16_t* vb) __attribute__((always_inline)) {
     const int2 rw = skey0 >= 32 && 2 * stp + 1 < nrows ? advance(rowA, 1) : rowA;  // uniform per wave
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < 4; ++u) {
       const int kx = skey0 + 4 * u;
       const uint32_t goff = (uint32_t)(((rw.x * a.Hp + rw.y) * a.Wp + A0 + (kx & 31)) * rbytes + h * D * 2 +
                                        chunk_slot(kx, lane & 15) * 16);
-      const int blk = 2 * wave + u;
+      const int blk = 4 * wave + u;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_ptr)(kb + blk * 512), 16, goff, 0, 0, 0);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_ptr)(vb + blk * 512), 16, goff, 0, 0, 0);
     }

@@ -296,7 +296,7 @@ vidax_status vidax_na3d_fwd(const void* q, const void* k, const void* v, void* o
   // 32-bit buffer offsets within one batch (plus a staged row past its end);
   // launch size
   if ((L + 32) * H * 256 > INT32_MAX) return VIDAX_ERR_UNSUPPORTED;
-  const int64_t nwg = (int64_t)B * H * ((grid_t + 1) / 2) * ((grid_h + 7) / 8) * ((grid_w + 15) / 16);
+  const int64_t nwg = (int64_t)B * H * ((grid_t + 1) / 2) * ((grid_h + 3) / 4) * ((grid_w + 15) / 16);
   if (nwg > INT32_MAX) return VIDAX_ERR_UNSUPPORTED;
   const hipError_t e =
       vidax::launch_na3d_fwd((const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, (uint16_t*)o, lse, B, H,
