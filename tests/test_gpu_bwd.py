@@ -153,6 +153,33 @@ def test_attn_bwd_scale_values(scale):
     _bwd_case(inputs.custom("bwd_scale", B=1, H=2, Lq=300, Lk=200, seed=38), scale=scale)
 
 
+def test_attn_bwd_workspace_holds_d():
+    """The first B * H * Lq values of the workspace hold D_i = <dO_i, O_i>
+    ([B, H, Lq]) on return, also for a batch without valid keys and for the
+    rows of a ragged last query tile: against the fp64 sum of the bf16
+    products, within the fp32 accumulation error (129 roundings of partial
+    sums bounded by sum |dO O|: 2^-17 of it)."""
+    import torch
+
+    w = [c for c in BWD if c.name == "bwd_cross"][0]
+    q, k, v, lv = inputs.make_qkv(w)
+    do = inputs.make_dout(w)
+    log(f"case workspace D {w.name}")
+    dec = oracle.bf16_bits_to_f64
+    ob, lse = _oracle_fwd_inputs(dec(q), dec(k), dec(v), w.scale, lv)
+    rows = w.B * w.H * w.Lq
+    ws = torch.full((rows,), float("nan"), dtype=torch.float32, device="cuda")
+    vx.attn_bwd(to_dev(q), to_dev(k), to_dev(v), to_dev(ob), to_dev(do), torch.from_numpy(lse).cuda(),
+                scale=w.scale, kv_valid_len=lengths_dev(lv), workspace=ws)
+    torch.cuda.synchronize()
+    got = ws.cpu().numpy().astype(np.float64).reshape(w.B, w.H, w.Lq)
+    prod = dec(do) * dec(ob)  # [B, Lq, H, d]
+    ref = prod.sum(axis=3).transpose(0, 2, 1)
+    bound = 2.0 ** -17 * np.abs(prod).sum(axis=3).transpose(0, 2, 1) + 1e-30
+    assert np.isfinite(got).all()
+    assert (np.abs(got - ref) <= bound).all(), float(np.max(np.abs(got - ref) / bound))
+
+
 def test_attn_bwd_split_matches_unsplit():
     """The same call with a workspace that holds only D (no query-stream
     split) and with the size vidax_attn_bwd_workspace_floats asks for (split
