@@ -4,7 +4,10 @@
 //
 // With a few key tiles per query tile, the query loads and output stores
 // (HBM) weigh as much as the products, and a kernel that streams them in and
-// out at query-tile boundaries spends most of its time waiting.  This form:
+// out at query-tile boundaries spends most of its time waiting.  Two forms,
+// one launch each: batches whose valid keys fit in three 64-key tiles run in
+// the resident form (described at its kernel below: the K/V of a head stay
+// in LDS), the others in the streaming form.  The streaming form:
 //   * runs one persistent workgroup per CU over a contiguous run of "items"
 //     (batch, head, 256-query tile), head by head so that the K/V of a head
 //     stays in the XCD's L2; the runs are balanced by key-tile steps, not by
@@ -49,6 +52,11 @@ constexpr int TILE = BN * D;  // elements of one K or V tile
 constexpr int BLK = 512;      // elements of one operand block
 constexpr int AREA = 32 * D;  // elements of one wave's staging area
 constexpr int kMemWaves = 4;
+// Batches whose valid keys fit in kResTiles tiles go to the resident form
+// (their K/V stay in LDS across the items of a head), the others to the
+// streaming form.
+constexpr int kResTiles = 3;
+__device__ __forceinline__ bool resident_batch(int lv) { return lv <= kResTiles * BN; }
 // Cache policy of the query loads and output stores: non-temporal.  Each
 // query row is read once and each output row written once; as streaming
 // accesses they do not displace the K/V tiles of the XCD's heads from the L2,
@@ -113,6 +121,11 @@ __global__ __launch_bounds__(NT) void xattn_kernel(XArgs a) {
     return __builtin_amdgcn_readfirstlane(l);
   };
   auto tiles_of = [&](int lv) __attribute__((always_inline)) { return max(1, (lv + BN - 1) / BN); };
+  // key-tile steps of an item of batch b in this form (0: the resident form's)
+  auto steps_of = [&](int b) __attribute__((always_inline)) {
+    const int lv = valid_len(b);
+    return resident_batch(lv) ? 0 : tiles_of(lv);
+  };
 
   // ---- this workgroup's run: the step stream is cut into G equal runs (at
   // item boundaries); XCD x owns a contiguous range of runs
@@ -120,12 +133,12 @@ __global__ __launch_bounds__(NT) void xattn_kernel(XArgs a) {
   const int run = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
   const long per_batch = (long)a.H * a.nqt;
   long total = 0;
-  for (int b = 0; b < a.B; ++b) total += per_batch * tiles_of(valid_len(b));
+  for (int b = 0; b < a.B; ++b) total += per_batch * steps_of(b);
   // first item whose first step is at or after step t, and that step
   auto item_at = [&](long t, long& first_step) __attribute__((always_inline)) {
     long cum = 0, base = 0;
     for (int b = 0; b < a.B; ++b) {
-      const long nt = tiles_of(valid_len(b));
+      const long nt = steps_of(b);
       const long steps = per_batch * nt;
       if (t < cum + steps) {
         const long i = (t - cum + nt - 1) / nt;
@@ -143,14 +156,15 @@ __global__ __launch_bounds__(NT) void xattn_kernel(XArgs a) {
   const long lid1 = item_at(total * (run + 1) / G, s1);
   if (lid0 >= lid1) return;
   int steps_left = (int)(s1 - s0);  // steps of the run from the current one on
-  int items_left = (int)(lid1 - lid0);
 
+  // the next item of this form (batches of the resident form are skipped)
   auto next_item = [&](Item& it) __attribute__((always_inline)) {
     if (++it.qt == a.nqt) {
       it.qt = 0;
       if (++it.h == a.H) {
         it.h = 0;
-        ++it.b;
+        do ++it.b;
+        while (it.b < a.B && resident_batch(valid_len(it.b)));
       }
     }
   };
@@ -399,7 +413,7 @@ __global__ __launch_bounds__(NT) void xattn_kernel(XArgs a) {
   n2 = n1;
   advance(n2);
   // item whose outputs are stored next; the queries loaded at the same time
-  // are those of the item two after it (valid while items_left > 1)
+  // are those of the item two after it (when the run holds that item)
   Item io = cur.it;
   Item qnext = cur.it;
   next_item(qnext);
@@ -412,7 +426,7 @@ __global__ __launch_bounds__(NT) void xattn_kernel(XArgs a) {
   read_q();
   __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
   __builtin_amdgcn_s_barrier();  // every wave has its queries out of the staging area
-  if (memw && items_left > 1) load_queries(qnext);
+  if (memw && steps_left > cur.nt) load_queries(qnext);
   if (!memw) {
     copy_k(cur, K0);
     if (steps_left > 1) copy_k(n1, K1);
@@ -446,7 +460,7 @@ __global__ __launch_bounds__(NT) void xattn_kernel(XArgs a) {
       store_outputs(io);
       next_item(io);
       __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-      if (items_left > 1) {
+      if (steps_left > ntc) {  // an item follows this one in the run
         Item qn = io;
         next_item(qn);
         load_queries(qn);
@@ -478,10 +492,7 @@ __global__ __launch_bounds__(NT) void xattn_kernel(XArgs a) {
     }
     if (!memw) __builtin_amdgcn_s_waitcnt(0);  // this wave's K/V copies have landed
     __builtin_amdgcn_s_barrier();
-    if (last) {
-      stored_any = true;
-      --items_left;
-    }
+    if (last) stored_any = true;
     jc = n1.j;
     ntc = n1.nt;
     lvc = n1.lv;
@@ -497,6 +508,343 @@ __global__ __launch_bounds__(NT) void xattn_kernel(XArgs a) {
   if (memw) store_outputs(io);
 }
 
+
+// ---- resident form: batches whose valid keys fit in kResTiles tiles.  The
+// K and V tiles of the current (batch, head) stay in LDS for all of its items
+// in the run (96 KB), so an item's key steps need no copies and no
+// barriers: the query/output traffic of the memory waves (the previous
+// item's outputs out, the next item's queries in, issued at the item's start)
+// runs beside the whole item's products, and nothing waits for it before the
+// next item's queries are read.  Barriers: one before those queries are read
+// (after the item's last scores), one after the outputs are staged, and one
+// after the K/V copies of a new head.  Log-sum-exps leave straight from
+// registers.  Same item order, run split (by key-tile steps of this form's
+// batches) and per-item arithmetic as the streaming form.
+__global__ __launch_bounds__(NT) void xattn_res_kernel(XArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t KS[kResTiles][TILE], VS[kResTiles][TILE];
+  __shared__ __attribute__((aligned(16))) uint16_t QO[NW * AREA];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool memw = wave < kMemWaves;
+  const int l32 = lane & 31;
+  const int hi = lane >> 5;
+  const int tok = a.H * D;
+  const int rbytes = tok * 2;
+
+  const __attribute__((address_space(4))) int32_t* lens =
+      (const __attribute__((address_space(4))) int32_t*)a.kv_valid_len;
+  auto valid_len = [&](int b) __attribute__((always_inline)) {
+    int l = a.Lk;
+    if (lens) l = min(max(lens[b], 0), a.Lk);
+    return __builtin_amdgcn_readfirstlane(l);
+  };
+  auto tiles_of = [&](int lv) __attribute__((always_inline)) { return max(1, (lv + BN - 1) / BN); };
+  auto steps_of = [&](int b) __attribute__((always_inline)) {
+    const int lv = valid_len(b);
+    return resident_batch(lv) ? tiles_of(lv) : 0;
+  };
+
+  // ---- this workgroup's run (as in the streaming form, over this form's steps)
+  const int G = gridDim.x;
+  const int run = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
+  const long per_batch = (long)a.H * a.nqt;
+  long total = 0;
+  for (int b = 0; b < a.B; ++b) total += per_batch * steps_of(b);
+  auto item_at = [&](long t, long& first_step) __attribute__((always_inline)) {
+    long cum = 0, base = 0;
+    for (int b = 0; b < a.B; ++b) {
+      const long nt = steps_of(b);
+      const long steps = per_batch * nt;
+      if (t < cum + steps) {
+        const long i = (t - cum + nt - 1) / nt;
+        first_step = cum + i * nt;
+        return base + i;
+      }
+      cum += steps;
+      base += per_batch;
+    }
+    first_step = cum;
+    return base;
+  };
+  long s0, s1;
+  const long lid0 = item_at(total * run / G, s0);
+  const long lid1 = item_at(total * (run + 1) / G, s1);
+  if (lid0 >= lid1) return;
+  int steps_left = (int)(s1 - s0);
+
+  auto next_item = [&](Item& it) __attribute__((always_inline)) {
+    if (++it.qt == a.nqt) {
+      it.qt = 0;
+      if (++it.h == a.H) {
+        it.h = 0;
+        do ++it.b;
+        while (it.b < a.B && !resident_batch(valid_len(it.b)));
+      }
+    }
+  };
+
+  // ---- queries in, outputs out (waves 0-3, staging areas wave and wave + 4)
+  uint16_t* const own = QO + wave * AREA;
+  int qvo[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) qvo[i] = (lane >> 4) * rbytes + stage_slot(lane & 15, 4 * i + (lane >> 4)) * 16;
+  auto rows_rsrc = [&](const uint16_t* base, const Item& it) __attribute__((always_inline)) {
+    const int row0 = it.qt * BM;
+    return __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(base + ((size_t)it.b * a.Lq + row0) * tok + (size_t)it.h * D), (short)0,
+        __builtin_amdgcn_readfirstlane(min(a.Lq - row0, BM) * rbytes), kBufferFlags);
+  };
+  auto load_queries = [&](const Item& it) __attribute__((always_inline)) {
+    const __amdgpu_buffer_rsrc_t rq = rows_rsrc(a.q, it);
+    const int rb = opaque(rbytes), w = opaque(wave);
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int area = w + kMemWaves * t;
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rq, (lds_ptr)(QO + area * AREA + 4 * i * D), 16, qvo[i & 3],
+                                                 (area * 32 + 4 * i) * rb, 0, kStreamPolicy);
+    }
+  };
+  auto store_outputs = [&](const Item& it) __attribute__((always_inline)) {
+    const __amdgpu_buffer_rsrc_t ro = rows_rsrc(a.o, it);
+    const int rb = opaque(rbytes), w = opaque(wave);
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int area = w + kMemWaves * t;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const u32x4 val =
+            *reinterpret_cast<const u32x4*>(QO + area * AREA + (4 * i + (lane >> 4)) * D + (lane & 15) * 8);
+        __builtin_amdgcn_raw_buffer_store_b128(val, ro, qvo[i & 3], (area * 32 + 4 * i) * rb, kStreamPolicy);
+      }
+    }
+  };
+  // log-sum-exps of the wave's 32 queries of item `it`
+  auto store_lse = [&](const Item& it, float v) __attribute__((always_inline)) {
+    const int row0 = it.qt * BM;
+    const __amdgpu_buffer_rsrc_t rl = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(a.lse ? a.lse + ((size_t)it.b * a.H + it.h) * a.Lq + row0 : a.lse), (short)0,
+        a.lse ? __builtin_amdgcn_readfirstlane(min(a.Lq - row0, BM) * 4) : 0, kBufferFlags);
+    if (hi == 0) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), rl, (wave * 32 + l32) * 4, 0, 0);
+  };
+
+  // ---- K/V tiles of a (batch, head): waves 0-3 copy the K tiles, waves 4-7
+  // the V tiles, wave w & 3 filling operand blocks 4 (w & 3) .. + 3 of each
+  // (the operand order of the streaming form's copies)
+  const int cw = wave & 3;
+  const int kvo = l32 * rbytes + hi * 16;
+  const int vvo = (8 * hi + 4 * ((lane >> 4) & 1) + ((lane & 7) >> 1)) * rbytes +
+                  2 * (16 * ((lane >> 3) & 1) + 8 * (lane & 1));
+  auto load_kv = [&](const Item& it, int lv, int nt) __attribute__((always_inline)) {
+    const int rb = opaque(rbytes), w = opaque(cw);
+    for (int j = 0; j < nt; ++j) {
+      const int rows = min(max(lv - j * BN, 0), BN);
+      const uint16_t* base = (memw ? a.k : a.v) + ((size_t)it.b * a.Lk + (size_t)j * BN) * tok + (size_t)it.h * D;
+      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+          (void*)base, (short)0, __builtin_amdgcn_readfirstlane(rows * rbytes), kBufferFlags);
+      if (memw) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)(KS[j] + (4 * w + t) * BLK), 16, kvo,
+                                                   32 * (t & 1) * rb + (2 * (2 * w + (t >> 1))) * 16, 0, 0);
+      } else {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr)(VS[j] + (4 * w + t) * BLK), 16, vvo,
+                                                   16 * w * rb + 64 * t, 0, 0);
+      }
+    }
+  };
+
+  // ---- compute (every wave: queries l32 of its staging area, lane halves hi)
+  bf16x8 qreg[8];
+  auto read_q = [&]() __attribute__((always_inline)) {
+    const uint32_t sgn = a.qsign < 0.f ? 0x80008000u : 0u;
+    const uint32_t keep = a.qsign == 0.f ? 0u : 0xffffffffu;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      u32x4 raw = *reinterpret_cast<const u32x4*>(own + l32 * D + stage_slot(2 * s + hi, l32) * 8);
+#pragma unroll
+      for (int p = 0; p < 4; ++p) raw[p] = (raw[p] ^ sgn) & keep;
+      qreg[s] = __builtin_bit_cast(bf16x8, raw);
+    }
+  };
+  const int koff = lane * 8;
+  const int voff = lane * 4;
+  auto qk = [&](const uint16_t* kb, f32x16 s[2]) __attribute__((always_inline)) {
+    s[0] = f32x16{};
+    s[1] = f32x16{};
+#pragma unroll
+    for (int st = 0; st < 8; ++st)
+#pragma unroll
+      for (int blk = 0; blk < 2; ++blk) {
+        const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kb + (2 * st + blk) * BLK + koff);
+        s[blk] = mfma32(kop, qreg[st], s[blk]);
+      }
+  };
+  f32x16 oacc[4];
+  float mref = -INFINITY;
+  float lsum = 0.f;
+  auto reset_acc = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) oacc[mb] = f32x16{};
+    mref = -INFINITY;
+    lsum = 0.f;
+  };
+  const float c2 = a.c2;
+  auto softmax_p = [&](const f32x16& s, bf16x8 pop[2]) __attribute__((always_inline)) {
+    const float nm = -mref;
+    float tsum = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      uint32_t pw[4];
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[8 * ks + e], c2, nm));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[8 * ks + e + 1], c2, nm));
+        pw[e >> 1] = pack_bf16x2(p0, p1);
+        tsum = dot2(pw[e >> 1], kOnesBf16x2, tsum);
+      }
+      pop[ks] = __builtin_bit_cast(bf16x8, make_uint4(pw[0], pw[1], pw[2], pw[3]));
+    }
+    return tsum;
+  };
+  auto block_max = [&](const f32x16& s) __attribute__((always_inline)) {
+    float m = fmaxf(s[0], s[1]);
+#pragma unroll
+    for (int i = 2; i < 16; ++i) m = fmaxf(m, s[i]);
+    return wave_half_max(m) * c2;
+  };
+  auto softmax_blk = [&](const f32x16& s, bf16x8 pop[2], bool first) __attribute__((always_inline)) {
+    if (first) {
+      const float m = block_max(s);
+      mref = m == -INFINITY ? 0.f : m;
+    }
+    float tsum = softmax_p(s, pop);
+    if (__builtin_amdgcn_ballot_w64(!(tsum < kSumLimit)) != 0) {
+      const float mnew = fmaxf(mref, block_max(s));
+      const float alpha = __builtin_amdgcn_exp2f(mref - mnew);
+      lsum *= alpha;
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) oacc[mb][i] *= alpha;
+      mref = mnew;
+      tsum = softmax_p(s, pop);
+    }
+    lsum += tsum;
+  };
+  auto pv_blk = [&](const uint16_t* vb, const bf16x8 pop[2], int blk) __attribute__((always_inline)) {
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+      const int ks = 2 * blk + k2;
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) {
+        const i16x4 lo = lds_read_tr16(vb + (4 * ks + mb) * BLK + voff);
+        const i16x4 hi4 = lds_read_tr16(vb + (4 * ks + mb) * BLK + BLK / 2 + voff);
+        const bf16x8 vop = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi4, 0, 1, 2, 3, 4, 5, 6, 7));
+        oacc[mb] = mfma32(vop, pop[k2], oacc[mb]);
+      }
+    }
+  };
+  auto mask_tail = [&](f32x16 s[2], int rem) __attribute__((always_inline)) {
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if (blk * 32 + 8 * (i >> 2) + 4 * hi + (i & 3) >= rem) s[blk][i] = -INFINITY;
+  };
+  auto stage_outputs = [&]() __attribute__((always_inline)) -> float {
+    const float l = wave_half_sum(lsum);
+    const bool ok = l > 0.f;
+    const float inv = ok ? 1.0f / l : 0.f;
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        u32x2 pk;
+        pk[0] = pack_bf16x2(oacc[mb][4 * g + 0] * inv, oacc[mb][4 * g + 1] * inv);
+        pk[1] = pack_bf16x2(oacc[mb][4 * g + 2] * inv, oacc[mb][4 * g + 3] * inv);
+        *reinterpret_cast<u32x2*>(own + l32 * D + stage_slot(4 * mb + g, l32) * 8 + 4 * hi) = pk;
+      }
+    return ok ? (mref + __log2f(l)) * 0.69314718055994531f : -INFINITY;
+  };
+
+  // ---- prologue: the first item's queries in registers, its head's K/V in
+  // LDS, the second item's queries on their way
+  Item it;
+  {
+    const int qt = (int)(lid0 % a.nqt);
+    const long bh = lid0 / a.nqt;
+    it = Item{qt, (int)(bh % a.H), (int)(bh / a.H)};
+  }
+  int lv = valid_len(it.b), nt = tiles_of(lv);
+  if (memw) load_queries(it);
+  load_kv(it, lv, nt);
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_s_barrier();
+  read_q();
+  __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+  __builtin_amdgcn_s_barrier();  // every wave has its queries out of the staging area
+  Item nx = it;
+  next_item(nx);
+  bool more = steps_left > nt;  // an item follows in the run
+  if (memw && more) load_queries(nx);
+
+  while (true) {
+    reset_acc();
+    f32x16 s[2];
+    for (int j = 0; j < nt; ++j) {
+      qk(KS[j], s);
+      if (j + 1 == nt) {
+        // the item's last scores are formed: the next item's queries into
+        // registers (they were loaded at this item's start)
+        if (more) {
+          if (memw) __builtin_amdgcn_s_waitcnt(0);
+          __builtin_amdgcn_s_barrier();
+          read_q();
+        }
+        if (lv < nt * BN) mask_tail(s, lv - j * BN);
+      }
+      bf16x8 pop0[2], pop1[2];
+      softmax_blk(s[0], pop0, j == 0);
+      pv_blk(VS[j], pop0, 0);
+      softmax_blk(s[1], pop1, false);
+      pv_blk(VS[j], pop1, 1);
+    }
+    store_lse(it, stage_outputs());
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);  // staging writes done before the barrier
+    __builtin_amdgcn_s_barrier();            // outputs staged; K/V of this item no longer read
+    if (!more) break;
+    const Item prev = it;
+    steps_left -= nt;
+    it = nx;
+    next_item(nx);
+    lv = valid_len(it.b);
+    nt = tiles_of(lv);
+    more = steps_left > nt;
+    const bool new_head = it.b != prev.b || it.h != prev.h;  // uniform
+    if (new_head) load_kv(it, lv, nt);
+    if (memw) {
+      // this item's outputs leave, the next item's queries come in
+      store_outputs(prev);
+      __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+      if (more) load_queries(nx);
+    }
+    if (new_head) {
+      // the K/V copies (issued before the query/output traffic) have landed
+      if (!memw) __builtin_amdgcn_s_waitcnt(0);
+      else if (more) __builtin_amdgcn_s_waitcnt(wait_vm(32));
+      else __builtin_amdgcn_s_waitcnt(wait_vm(16));
+      __builtin_amdgcn_s_barrier();
+    }
+  }
+  if (memw) store_outputs(it);
+}
+
 }  // namespace
 
 hipError_t launch_xattn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, uint16_t* o, float* lse,
@@ -508,7 +856,15 @@ hipError_t launch_xattn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t
   a.nqt = (Lq + BM - 1) / BM;
   a.c2 = scale == 0.f ? 1.f : fabsf(scale) * 1.4426950408889634f;
   a.qsign = scale > 0.f ? 1.f : (scale < 0.f ? -1.f : 0.f);
-  return launch_kernel(xattn_kernel, (unsigned)(8 * ((cus + 7) / 8)), (unsigned)NT, stream, a);
+  const unsigned g = (unsigned)(8 * ((cus + 7) / 8));
+  // batches with at most kResTiles key tiles (none without per-batch lengths
+  // when Lk exceeds them), then the others (none when every batch fits)
+  const bool short_keys = Lk <= kResTiles * BN;
+  if (short_keys || kv_valid_len) {
+    const hipError_t e = launch_kernel(xattn_res_kernel, g, (unsigned)NT, stream, a);
+    if (e != hipSuccess || short_keys) return e;
+  }
+  return launch_kernel(xattn_kernel, g, (unsigned)NT, stream, a);
 }
 
 }  // namespace vidax
