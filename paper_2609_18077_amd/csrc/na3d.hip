@@ -177,21 +177,27 @@ __global__ __launch_bounds__(NT, 2) void na3d_fwd_kernel(NaArgs a) {
     }
     return r;
   };
-  // staging: wave w copies 1 KB blocks 2 w, 2 w + 1 of each tensor, 4 keys a
-  // block (keys 0 .. 31 from the step's first row, 32 .. 63 from its second,
-  // at w positions A0 .. A0 + 31; a missing second row repeats the first);
-  // lane i fills slot i & 15 of key 4 blk + (i >> 4)
-  const int skey0 = 16 * wave + (lane >> 4);  // block 4 w; block 4 w + u is key + 4 u
+  // staging: wave w copies 1 KB blocks 4 w .. 4 w + 3 of each tensor, 4 keys
+  // a block (keys 0 .. 31 from the step's first row -- waves 0, 1 --, 32 .. 63
+  // from its second -- waves 2, 3 --, at w positions A0 .. A0 + 31; a missing
+  // second row repeats the first); lane i fills slot i & 15 of key
+  // 4 blk + (i >> 4).  The lane's byte offset within the staged row span is
+  // fixed (cg); the row's base is a uniform offset.
+  const bool second = wave >= 2;  // uniform
+  int cg[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int kx = 16 * wave + (lane >> 4) + 4 * u;
+    cg[u] = (kx & 31) * rbytes + h * D * 2 + chunk_slot(kx, lane & 15) * 16;
+  }
   auto stage = [&](int stp, int2 rowA, uint16_t* kb, uint16_t* vb) __attribute__((always_inline)) {
-    const int2 rw = skey0 >= 32 && 2 * stp + 1 < nrows ? advance(rowA, 1) : rowA;  // uniform per wave
+    const int2 rw = second && 2 * stp + 1 < nrows ? advance(rowA, 1) : rowA;
+    const int rbase = __builtin_amdgcn_readfirstlane(((rw.x * a.Hp + rw.y) * a.Wp + A0) * rbytes);
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const int kx = skey0 + 4 * u;
-      const uint32_t goff = (uint32_t)(((rw.x * a.Hp + rw.y) * a.Wp + A0 + (kx & 31)) * rbytes + h * D * 2 +
-                                       chunk_slot(kx, lane & 15) * 16);
       const int blk = 4 * wave + u;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_ptr)(kb + blk * 512), 16, goff, 0, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_ptr)(vb + blk * 512), 16, goff, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_ptr)(kb + blk * 512), 16, cg[u], rbase, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_ptr)(vb + blk * 512), 16, cg[u], rbase, 0, 0);
     }
   };
 
