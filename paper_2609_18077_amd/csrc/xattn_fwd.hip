@@ -134,16 +134,20 @@ __global__ __launch_bounds__(NT) void xattn_kernel(XArgs a) {
   const long per_batch = (long)a.H * a.nqt;
   long total = 0;
   for (int b = 0; b < a.B; ++b) total += per_batch * steps_of(b);
-  // first item whose first step is at or after step t, and that step
+  // first item of this form whose first step is at or after step t, and
+  // that step (past the last item of a batch: the first item of the next
+  // batch of this form)
   auto item_at = [&](long t, long& first_step) __attribute__((always_inline)) {
     long cum = 0, base = 0;
     for (int b = 0; b < a.B; ++b) {
       const long nt = steps_of(b);
       const long steps = per_batch * nt;
-      if (t < cum + steps) {
-        const long i = (t - cum + nt - 1) / nt;
-        first_step = cum + i * nt;
-        return base + i;
+      if (nt > 0 && t < cum + steps) {
+        const long i = t <= cum ? 0 : (t - cum + nt - 1) / nt;
+        if (i < per_batch) {
+          first_step = cum + i * nt;
+          return base + i;
+        }
       }
       cum += steps;
       base += per_batch;
@@ -557,10 +561,12 @@ __global__ __launch_bounds__(NT) void xattn_res_kernel(XArgs a) {
     for (int b = 0; b < a.B; ++b) {
       const long nt = steps_of(b);
       const long steps = per_batch * nt;
-      if (t < cum + steps) {
-        const long i = (t - cum + nt - 1) / nt;
-        first_step = cum + i * nt;
-        return base + i;
+      if (nt > 0 && t < cum + steps) {
+        const long i = t <= cum ? 0 : (t - cum + nt - 1) / nt;
+        if (i < per_batch) {
+          first_step = cum + i * nt;
+          return base + i;
+        }
       }
       cum += steps;
       base += per_batch;

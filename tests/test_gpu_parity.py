@@ -425,11 +425,16 @@ def _convex_bounds_ok(ob, v, lv, heads):
 
 
 # Short key sequences without rotation at more than four query tiles per CU
-# run as one persistent workgroup per CU looping over tiles: empty batches
-# (Lv = 0), a ragged last query tile, Lk at the persistent-form limit.
+# run as one persistent workgroup per CU looping over tiles (two forms:
+# batches with at most 192 valid keys keep their K/V in LDS, the others
+# stream them): empty batches (Lv = 0), a ragged last query tile, Lk at the
+# persistent-form limit, and batches of the two forms alternating (each
+# form's runs then skip the other's batches), at the 192-key boundary.
 PERSISTENT = [
     inputs.custom("persist_empty_batch", B=2, H=8, Lq=20000, Lk=300, seed=31, kv_valid=("fixed", [0, 173])),
     inputs.custom("persist_long_keys", B=1, H=16, Lq=17000, Lk=2048, seed=32),
+    inputs.custom("persist_alternating", B=5, H=8, Lq=7000, Lk=512, seed=33,
+                  kv_valid=("fixed", [100, 400, 192, 193, 1])),
 ]
 
 
