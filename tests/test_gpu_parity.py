@@ -435,6 +435,8 @@ PERSISTENT = [
     inputs.custom("persist_long_keys", B=1, H=16, Lq=17000, Lk=2048, seed=32),
     inputs.custom("persist_alternating", B=5, H=8, Lq=7000, Lk=512, seed=33,
                   kv_valid=("fixed", [100, 400, 192, 193, 1])),
+    # every batch short and no per-batch lengths: the resident form alone
+    inputs.custom("persist_short_nolen", B=1, H=16, Lq=17000, Lk=150, seed=34),
 ]
 
 
