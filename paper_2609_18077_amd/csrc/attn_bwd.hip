@@ -193,18 +193,18 @@ __device__ __forceinline__ void dq_body(const BwdArgs& a) {
   {
     bf16x8 oop[8];
     own_operand(a.o + rowoff, qlive, hi, oop);
-    float sum = 0.f;
+    // packed bf16 pair products, two fp32 chains
+    float sum[2] = {0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       const uint4 x = __builtin_bit_cast(uint4, dop[s]), y = __builtin_bit_cast(uint4, oop[s]);
       const uint32_t xw[4] = {x.x, x.y, x.z, x.w}, yw[4] = {y.x, y.y, y.z, y.w};
 #pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        sum = fmaf(bf16lo_to_f32(xw[p]), bf16lo_to_f32(yw[p]), sum);
-        sum = fmaf(bf16hi_to_f32(xw[p]), bf16hi_to_f32(yw[p]), sum);
-      }
+      for (int p = 0; p < 4; ++p)
+        sum[p & 1] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, xw[p]), __builtin_bit_cast(bf16x2, yw[p]),
+                                                     sum[p & 1], false);
     }
-    dl = half_sum(sum);
+    dl = half_sum(sum[0] + sum[1]);
     if (qlive && hi == 0) a.delta[lrow] = dl;
   }
   f32x16 acc[4];
