@@ -477,6 +477,44 @@ def test_persistent_short_keys_sampled(w):
     assert _convex_bounds_ok(ob, v, lv, list(range(w.H)))
 
 
+def test_batch_at_the_2gib_limit():
+    """One batch of q, k, v and o just below 2 GiB, the largest the forward
+    accepts (max(Lq, Lk) * H * d * 2 <= 2^31 - 1 - 4096): B=1, H=64,
+    L=131071; element (n, h) sits at byte (n * 64 + h) * 256, so the last rows
+    of the last head are at the top of the 32-bit offset range.  The dense
+    kernel (Lq = Lk, no rotation) and the short-key resident form (the first
+    64 keys, 50 valid).  Inputs are seeded N(0, 1) drawn on the GPU (torch's
+    generator) and copied back for the heads the oracle checks: sampled rows,
+    the last ones included, of the first and last head."""
+    import torch
+
+    B, H, L = 1, 64, 131071
+    assert L * H * 128 * 2 <= 2 ** 31 - 1 - 4096 < (L + 1) * H * 128 * 2
+    g = torch.Generator(device="cuda")
+    g.manual_seed(41)
+    mk = lambda n: torch.randn((B, n, H, 128), generator=g, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    q, k, v = mk(L), mk(L), mk(L)
+    scale = float(np.float32(1 / np.sqrt(128)))
+    hs = [0, H - 1]
+    rows = np.array([0, 1, 255, 256, 65535, 130815, 130816, 131040, 131069, 131070])
+    bits = lambda t: t[:, :, hs].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    dec = oracle.bf16_bits_to_f64
+    qh = dec(bits(q))
+    for name, lk, lens in (("dense", L, None), ("short keys", 64, [50])):
+        log(f"case 2 GiB limit, {name}: B{B} H{H} Lq{L} Lk{lk} lens={lens}")
+        kk, vv = (k, v) if lk == L else (k[:, :lk].contiguous(), v[:, :lk].contiguous())
+        o, lse = vx.attn_fwd(q, kk, vv, scale=scale, kv_valid_len=lengths_dev(lens), return_lse=True)
+        torch.cuda.synchronize()
+        ob = bits(o)[:, rows]
+        lb = lse[:, hs].cpu().numpy()[:, :, rows]
+        ro, rl = oracle.attn_ref_rows(qh, dec(bits(kk)), dec(bits(vv)), scale, rows, kv_valid_len=lens, workers=8)
+        assert_parity(ob, ro, f"2 GiB limit, {name}")
+        assert_lse(lb, rl, f"2 GiB limit, {name}")
+        del o, lse, kk, vv
+    del q, k, v
+    torch.cuda.empty_cache()
+
+
 def test_full_size_prerotated_wan13b_sampled():
     import dataclasses
 
