@@ -149,9 +149,28 @@ class Telemetry:
                           "averages: the SQ counters of the profiles give the shader clock under this load"}
 
 
-def time_gpu(w, steps, warmup, fused=False, telemetry=False):
+def warm_up(fn, seconds=0.3):
+    """Untimed calls of `fn` until `seconds` have passed.  The engine clock
+    drops while the host prepares a workload's inputs and needs tens of
+    milliseconds of load to come back; a few short calls do not cover that."""
+    import torch
+
+    until = time.perf_counter() + seconds
+    while True:
+        for _ in range(4):
+            fn()
+        torch.cuda.synchronize()
+        if time.perf_counter() >= until:
+            return
+
+
+def time_gpu(w, steps, warmup, fused=False, telemetry=False, warm_s=0.0):
     """Times `steps` steps.  Events bracket the attention launch of each step
-    (on the stream it runs on); the wall clock covers the whole step."""
+    (on the stream it runs on); the wall clock covers the whole step.  After
+    the `warmup` steps, further untimed steps run until `warm_s` seconds have
+    passed: the engine clock drops while the host generates a workload's
+    inputs and takes tens of milliseconds of load to come back, which a few
+    sub-millisecond calls do not cover."""
     import dataclasses
 
     import torch
@@ -190,6 +209,12 @@ def time_gpu(w, steps, warmup, fused=False, telemetry=False):
         prologue()
         attention()
     torch.cuda.synchronize()
+    warm_until = time.perf_counter() + warm_s
+    while time.perf_counter() < warm_until:
+        for _ in range(8):
+            prologue()
+            attention()
+        torch.cuda.synchronize()
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
     torch.cuda.synchronize()
@@ -237,9 +262,7 @@ def time_prologues(w, steps):
     out = {}
     for name, fn in [("rope3d_" + w.name, lambda: vx.rope3d(x, rope, out=y)),
                      ("qk_norm_rope_" + w.name, lambda: vx.qk_norm_rope(x, rope, gain=g, out=y))]:
-        for _ in range(3):
-            fn()
-        torch.cuda.synchronize()
+        warm_up(fn)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
         for _ in range(steps):
@@ -270,9 +293,7 @@ def time_backward(w, steps):
     lvd = None if lv is None else torch.from_numpy(np.asarray(lv, dtype=np.int32)).cuda()
     o, lse = vx.attn_fwd(q, k, v, scale=w.scale, kv_valid_len=lvd, return_lse=True)
     fn = lambda: vx.attn_bwd(q, k, v, o, do, lse, scale=w.scale, kv_valid_len=lvd)
-    for _ in range(2):
-        fn()
-    torch.cuda.synchronize()
+    warm_up(fn)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(steps):
@@ -315,9 +336,7 @@ def time_na3d(w, steps):
     q, k, v = (torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16) for x in inputs.make_na_qkv(w))
     o = torch.empty_like(q)
     fn = lambda: vx.na3d_fwd(q, k, v, w.grid, w.window, w.border, scale=w.scale, out=o)
-    for _ in range(3):
-        fn()
-    torch.cuda.synchronize()
+    warm_up(fn)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(steps):
@@ -346,9 +365,7 @@ def time_qkv_proj(w, steps):
     xd, wd, bd, gqd, gkd = bf(x), bf(wt), f32(bias), f32(gq), f32(gk)
     rope = vx.Rope(w.grid, w.dims, w.theta) if w.grid is not None else None
     fn = lambda: vx.qkv_proj(xd, wd, w.B, w.L, w.H, bias=bd, gain_q=gqd, gain_k=gkd, eps=w.eps, rope=rope)
-    for _ in range(20):  # also lets the clock settle when this is the first kernel of the process
-        fn()
-    torch.cuda.synchronize()
+    warm_up(fn)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(steps):
@@ -383,7 +400,7 @@ def time_cold(w, steps):
     o = torch.empty_like(qd)
     scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
     fn = lambda: vx.attn_fwd(qd, kd, vd, scale=w.scale, kv_valid_len=ld, out=o)
-    fn()
+    warm_up(lambda: (scratch.fill_(1), fn()))
     per = []
     for _ in range(steps):
         scratch.fill_(1)
@@ -549,7 +566,7 @@ def main():
             if name == w.name:
                 continue
             n = 5 if ww.Lq * ww.Lk * ww.H * ww.B > 2e10 else max(5, args.steps // 2)
-            rr = time_gpu(ww, n, 3)
+            rr = time_gpu(ww, n, 3, warm_s=0.3)
             _, _, _, lvw = rr.pop("inputs")
             f2 = flops(ww, lvw)
             t = rr["event_ms_mean"] * 1e-3
