@@ -425,17 +425,22 @@ def _convex_bounds_ok(ob, v, lv, heads):
 
 
 # Short key sequences without rotation at more than four query tiles per CU
-# run as one persistent workgroup per CU looping over tiles (two forms:
-# batches with at most 192 valid keys keep their K/V in LDS, the others
-# stream them): empty batches (Lv = 0), a ragged last query tile, Lk at the
-# persistent-form limit, and batches of the two forms alternating (each
-# form's runs then skip the other's batches), at the 192-key boundary.
+# run as one persistent workgroup per CU looping over query tiles; three K/V
+# tile buffers keep the last tiles of a head between its query tiles, and a
+# query tile with more than three key tiles copies the others as it goes (in
+# an order that depends on the tiles kept from the query tile before): empty
+# batches (Lv = 0), a ragged last query tile, Lk at the persistent-form limit
+# (32 tiles), batches of 2, 7, 3, 4 and 1 tiles in turn (the 192/193-key
+# boundary between copying and not), of 5, 6 and 8 tiles (every tile count
+# mod 3; partial and full last tiles), and a case without per-batch lengths
+# where no query tile copies.
 PERSISTENT = [
     inputs.custom("persist_empty_batch", B=2, H=8, Lq=20000, Lk=300, seed=31, kv_valid=("fixed", [0, 173])),
     inputs.custom("persist_long_keys", B=1, H=16, Lq=17000, Lk=2048, seed=32),
     inputs.custom("persist_alternating", B=5, H=8, Lq=7000, Lk=512, seed=33,
                   kv_valid=("fixed", [100, 400, 192, 193, 1])),
-    # every batch short and no per-batch lengths: the resident form alone
+    inputs.custom("persist_tile_counts", B=4, H=8, Lq=9000, Lk=512, seed=35,
+                  kv_valid=("fixed", [257, 384, 449, 512])),
     inputs.custom("persist_short_nolen", B=1, H=16, Lq=17000, Lk=150, seed=34),
 ]
 
@@ -482,8 +487,8 @@ def test_batch_at_the_2gib_limit():
     accepts (max(Lq, Lk) * H * d * 2 <= 2^31 - 1 - 4096): B=1, H=64,
     L=131071; element (n, h) sits at byte (n * 64 + h) * 256, so the last rows
     of the last head are at the top of the 32-bit offset range.  The dense
-    kernel (Lq = Lk, no rotation) and the short-key resident form (the first
-    64 keys, 50 valid).  Inputs are seeded N(0, 1) drawn on the GPU (torch's
+    kernel (Lq = Lk, no rotation) and the short-key kernel (the first 64
+    keys, 50 valid).  Inputs are seeded N(0, 1) drawn on the GPU (torch's
     generator) and copied back for the heads the oracle checks: sampled rows,
     the last ones included, of the first and last head."""
     import torch
