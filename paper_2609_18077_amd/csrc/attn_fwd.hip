@@ -173,7 +173,7 @@ constexpr int TILE = BN * D;  // elements per K or V tile
 constexpr int BLK = 512;      // elements per operand block
 // Short key sequences without rotation: at or below this many keys (and with
 // enough query tiles to fill the chip) the persistent short-key kernel runs.
-constexpr int kAttnShortKeys = 2048;
+constexpr int kAttnShortKeys = 1024;
 
 // ROPE: rotate the queries (and build the table); ROPE_K: also rotate the keys
 // while staging them (false when the caller passes pre-rotated keys).
@@ -616,13 +616,26 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   };
 
   // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
-  // contiguous range of logical tiles so the query tiles of one (b, h)
-  // share that XCD's L2 for the K/V stream.
+  // contiguous range of positions so the query tiles of one (b, h) share
+  // that XCD's L2 for the K/V stream.  The positions run over the eighths of
+  // every batch in turn (eighth 0 of batch 0, of batch 1, ..., eighth 1 of
+  // batch 0, ...), so that each XCD gets about an eighth of every batch:
+  // batches of different valid lengths then load the XCDs evenly (with
+  // batch after batch, the XCDs holding the longer batches finished last).
+  // One batch: position = logical tile.
   int lid;
   {
     const int i = blockIdx.x, n = a.nwg;
     const int per = n >> 3, rem = n & 7, xcd = i & 7, kk = i >> 3;
-    lid = xcd < rem ? xcd * (per + 1) + kk : rem * (per + 1) + (xcd - rem) * per + kk;
+    const int pos = xcd < rem ? xcd * (per + 1) + kk : rem * (per + 1) + (xcd - rem) * per + kk;
+    const int N = a.nwg / a.B;  // tiles per batch: eighth c holds p + (c < r) of them
+    const int p = N >> 3, r = N & 7;
+    const int big = a.B * r * (p + 1);  // positions in the eighths of size p + 1
+    const int c = pos < big ? pos / (a.B * (p + 1)) : r + (pos - big) / (a.B * p);
+    const int sc = c < r ? p + 1 : p;
+    const int cs = c * p + min(c, r);  // start of eighth c within a batch
+    const int rm = pos - a.B * cs;
+    lid = (rm / sc) * N + cs + rm % sc;
   }
   begin_tile(lid);
   reset_acc();
