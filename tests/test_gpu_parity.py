@@ -430,13 +430,13 @@ def _convex_bounds_ok(ob, v, lv, heads):
 # query tile with more than three key tiles copies the others as it goes (in
 # an order that depends on the tiles kept from the query tile before): empty
 # batches (Lv = 0), a ragged last query tile, Lk at the persistent-form limit
-# (32 tiles), batches of 2, 7, 3, 4 and 1 tiles in turn (the 192/193-key
+# (1024 keys, 16 tiles), batches of 2, 7, 3, 4 and 1 tiles in turn (the 192/193-key
 # boundary between copying and not), of 5, 6 and 8 tiles (every tile count
 # mod 3; partial and full last tiles), and a case without per-batch lengths
 # where no query tile copies.
 PERSISTENT = [
     inputs.custom("persist_empty_batch", B=2, H=8, Lq=20000, Lk=300, seed=31, kv_valid=("fixed", [0, 173])),
-    inputs.custom("persist_long_keys", B=1, H=16, Lq=17000, Lk=2048, seed=32),
+    inputs.custom("persist_long_keys", B=1, H=16, Lq=17000, Lk=1024, seed=32),
     inputs.custom("persist_alternating", B=5, H=8, Lq=7000, Lk=512, seed=33,
                   kv_valid=("fixed", [100, 400, 192, 193, 1])),
     inputs.custom("persist_tile_counts", B=4, H=8, Lq=9000, Lk=512, seed=35,
@@ -447,7 +447,7 @@ PERSISTENT = [
 
 def _random_persistent(n=6, seed=2027):
     """Seeded random shapes that reach the short-key kernel: no rotation,
-    Lk <= 2048, ragged Lq, per-batch valid lengths (some 0, some past Lk,
+    Lk <= 1024, ragged Lq, per-batch valid lengths (some 0, some past Lk,
     some not a multiple of the 64-key tile) and more than 4 query tiles per
     CU (B * H * ceil(Lq / 256) > 1024)."""
     rng = np.random.default_rng(seed)
@@ -455,7 +455,7 @@ def _random_persistent(n=6, seed=2027):
     for i in range(n):
         B = int(rng.integers(1, 5))
         H = int(rng.integers(4, 17))
-        Lk = int(rng.choice([1, 63, 64, 65, 300, 512, 777, 2048]))
+        Lk = int(rng.choice([1, 63, 64, 65, 300, 512, 777, 1024]))
         need = 1024 // (B * H) + 2  # query tiles per (b, h) beyond the threshold
         Lq = int(rng.integers(need * 256 - 255, need * 256 + 3000))
         lens = [int(x) for x in rng.integers(-3, Lk + 40, B)]
