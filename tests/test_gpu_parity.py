@@ -224,6 +224,10 @@ RAGGED = [
     inputs.custom("few", B=1, H=1, Lq=5, Lk=3, seed=24),
     inputs.custom("one", B=2, H=1, Lq=1, Lk=1, seed=25),
     inputs.custom("tile_plus_one", B=1, H=2, Lq=257, Lk=65, seed=26, grid=(1, 5, 13)),
+    # dense kernel, batches of very different valid lengths: 60 query tiles a
+    # batch, so each XCD's run holds a part of every batch (eighths of 8 and
+    # 7 tiles) and the position -> tile map is exercised past its one-batch case
+    inputs.custom("mixed_lengths", B=3, H=5, Lq=3000, Lk=2500, seed=27, kv_valid=("fixed", [2500, 70, 1900])),
 ]
 
 
