@@ -115,9 +115,9 @@ vidax_status vidax_rope3d_transpose(const void* x, void* y, int32_t B, int32_t L
  *   gain : fp32 [d] on the device, shared by all heads, 16-byte aligned; or
  *          NULL for unit gain.
  *   eps  : >= 0 and finite (e.g. 1e-6); an all-zero row with eps = 0 gives NaN.
- *   rope : host pointer to a descriptor (as vidax_rope3d; pair_mode 0 only,
- *          VIDAX_ERR_UNSUPPORTED otherwise; keys_prerotated is ignored), or
- *          NULL for normalisation and gain only.
+ *   rope : host pointer to a descriptor (as vidax_rope3d, either pair_mode;
+ *          keys_prerotated is ignored), or NULL for normalisation and gain
+ *          only.
  * Requires d == 128 (VIDAX_ERR_UNSUPPORTED otherwise); B, L, H >= 0
  * (zero-sized calls are no-ops).  HBM-bound: one read and one write of x.
  */
@@ -142,10 +142,11 @@ vidax_status vidax_qk_norm_rope(const void* x, void* y, const float* gain, float
  *          with the same descriptor (vidax_rope3d): every query tile of a
  *          head re-rotates every key tile in the fused form, so one
  *          vidax_rope3d pass over k is cheaper at long sequence lengths.
- *          Requires pair_mode 0, grid_t, grid_h, grid_w <= 1023, a rotary
- *          table of at most 4096 entries (VIDAX_ERR_UNSUPPORTED otherwise) and
- *          grid_t*grid_h*grid_w <= min(Lq, Lk); the half-split convention is
- *          served by rotating q and k with vidax_rope3d and passing rope = NULL.
+ *          Half-split pairs (pair_mode 1) require keys_prerotated = 1 (the
+ *          fused key rotation pairs interleaved channels).  Requires grid_t,
+ *          grid_h, grid_w <= 1023, a rotary table of at most 4096 entries
+ *          (VIDAX_ERR_UNSUPPORTED otherwise) and grid_t*grid_h*grid_w <=
+ *          min(Lq, Lk).
  *   All Lq rows are computed; there is no causal mask.  Matrix products run
  *   on bf16 inputs with fp32 accumulation; the softmax is fp32.
  *   Requires d == 128; o must not alias q, k or v.  B, H, Lq, Lk >= 0.

@@ -255,11 +255,29 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
 
   // ---- Q: lane holds query qrow, d-chunks 2s + hi (s = 0..7) as MFMA B operands
   bf16x8 qreg[8];
+  // Half-split pairs (keys then come rotated by vidax_rope3d): channel ch of
+  // the block of axis a (offset o_a, width d_a) pairs with ch +- d_a / 2,
+  // which another lane holds; it is read from the query row still in the
+  // staging area.  Returns the rotated, scaled channel ch of the lane's query.
+  auto half_split_q = [&](int ch, float x, uint32_t qpos, float qm) __attribute__((always_inline)) {
+    const RopeParams& r = a.rp;
+    int o, hl, pb;  // block offset, half width, pairs of the blocks before it
+    if (ch < r.dt) { o = 0; hl = r.dt >> 1; pb = 0; }
+    else if (ch < r.dt + r.dh) { o = r.dt; hl = r.dh >> 1; pb = r.dt >> 1; }
+    else { o = r.dt + r.dh; hl = r.dw >> 1; pb = (r.dt >> 1) + (r.dh >> 1); }
+    const bool first = ch - o < hl;
+    const int j = first ? ch - o : ch - o - hl;
+    const int pc = first ? ch + hl : ch - hl;
+    const float xp = __uint_as_float((uint32_t)stage[l32 * D + stage_slot(pc >> 3, l32) * 8 + (pc & 7)] << 16);
+    const float2 cs = table_entry(tab, pair_idx(a, pb + j), qpos);
+    return (first ? fmaf(x, cs.x, -xp * cs.y) : fmaf(xp, cs.y, x * cs.x)) * qm;
+  };
   auto make_q = [&](const uint4 raw[8]) __attribute__((always_inline)) {
     const uint32_t qpos = ROPE ? packed_pos(a, qlive ? qrow : a.rp.n_rot) : 0u;
     const float qm = a.qmul;
     const uint32_t sgn = a.qsign < 0.f ? 0x80008000u : 0u;
     const uint32_t keep = a.qsign == 0.f ? 0u : 0xffffffffu;
+    const bool half = ROPE && a.rp.pair_mode != 0;  // uniform
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       const int c = 2 * s + hi;
@@ -268,8 +286,12 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
       for (int p = 0; p < 4; ++p) {
         if (ROPE) {  // rotated and scaled in fp32, rounded once
           const float x0 = bf16lo_to_f32(wq[p]), x1 = bf16hi_to_f32(wq[p]);
-          const float2 cs = table_entry(tab, pair_idx(a, 4 * c + p), qpos);
-          wq[p] = pack_bf16x2(fmaf(x0, cs.x, -x1 * cs.y) * qm, fmaf(x0, cs.y, x1 * cs.x) * qm);
+          if (half) {
+            wq[p] = pack_bf16x2(half_split_q(8 * c + 2 * p, x0, qpos, qm), half_split_q(8 * c + 2 * p + 1, x1, qpos, qm));
+          } else {
+            const float2 cs = table_entry(tab, pair_idx(a, 4 * c + p), qpos);
+            wq[p] = pack_bf16x2(fmaf(x0, cs.x, -x1 * cs.y) * qm, fmaf(x0, cs.y, x1 * cs.x) * qm);
+          }
         } else {  // exact: sign only
           wq[p] = (wq[p] ^ sgn) & keep;
         }
@@ -667,7 +689,8 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
 
 bool attn_rope_supported(const RopeParams& rp) {
   if (!rp.enabled) return true;
-  if (rp.pair_mode != 0) return false;
+  // half-split pairs: queries only (the fused key rotation pairs interleaved channels)
+  if (rp.pair_mode != 0 && !rp.keys_prerotated) return false;
   if (rp.gw > kAttnGridHWMax || rp.gh > kAttnGridHWMax || rp.gt > kAttnGridTMax) return false;
   const long entries = (long)(rp.gt + 1) * (rp.dt / 2) + (long)(rp.gh + 1) * (rp.dh / 2) + (long)(rp.gw + 1) * (rp.dw / 2);
   return entries <= kAttnTableMax;

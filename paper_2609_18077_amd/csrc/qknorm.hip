@@ -1,6 +1,6 @@
 // Query/key prologue, bf16 [B, L, H, 128] -> bf16 (HBM-bound): per-(token,
 // head) RMS normalisation in fp32, a per-channel gain shared by all heads, the
-// 3D rotation (interleaved pairs), rounding to bf16.
+// 3D rotation (interleaved or half-split pairs), rounding to bf16.
 //
 // Layout as in the standalone rotary kernel: the 16 channel chunks (16 B)
 // of a (token, head) row go to 16 consecutive lanes; a lane holds the four
@@ -10,7 +10,11 @@
 // squares is combined across its 16 lanes with data-parallel lane moves
 // (rotations within the 16-lane row, then permutations within quads), so
 // each lane ends with the row total without touching LDS.  Every lane reads
-// its chunk before any lane of the row writes, so y may alias x.
+// its chunk before any lane of the row writes, so y may alias x.  With
+// half-split pairs a channel's partner (d_a / 2 further in its axis block)
+// sits in another lane: the row's normalised fp32 values pass through a
+// per-row LDS buffer of the 16 lanes (one wave's lanes, so no barrier), and
+// each lane forms the angles of its 8 channels rather than of 4 pairs.
 #include "launch.hpp"
 
 namespace vidax {
@@ -38,9 +42,10 @@ __device__ __forceinline__ float row16_sum(float v) {
   return v;
 }
 
-template <bool ROPE>
+template <bool ROPE, bool HALF>
 __global__ __launch_bounds__(kThreads) void qk_norm_kernel(QkNormArgs a) {
   const RopeParams& rp = a.rp;
+  __shared__ float rowbuf[HALF ? kThreads * 8 : 1];  // half split: 128 channels of each lane group's row
 
   const int c = threadIdx.x & 15;  // chunk: channels 8c .. 8c + 7 = pairs 4c .. 4c + 3
   float g[8];
@@ -54,7 +59,25 @@ __global__ __launch_bounds__(kThreads) void qk_norm_kernel(QkNormArgs a) {
   }
   PairSlot slot[4];
   float omega[4];  // frequency of each pair of the chunk
-  if (ROPE) {
+  // half split: per channel e of the chunk, its axis, frequency, whether it
+  // is the first of its pair, and where its partner lies in the row buffer
+  int hax[8], hpart[8];
+  bool hfirst[8];
+  float homega[8];
+  if (HALF) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int ch = 8 * c + e;
+      int o, hl;
+      if (ch < rp.dt) { o = 0; hl = rp.dt >> 1; hax[e] = 0; }
+      else if (ch < rp.dt + rp.dh) { o = rp.dt; hl = rp.dh >> 1; hax[e] = 1; }
+      else { o = rp.dt + rp.dh; hl = rp.dw >> 1; hax[e] = 2; }
+      hfirst[e] = ch - o < hl;
+      const int j = hfirst[e] ? ch - o : ch - o - hl;
+      hpart[e] = hfirst[e] ? ch + hl : ch - hl;
+      homega[e] = exp2f(-((float)(2 * j) / (float)(2 * hl)) * rp.log2_theta);
+    }
+  } else if (ROPE) {
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
       slot[p] = pair_slot(rp, 4 * c + p);
@@ -70,17 +93,29 @@ __global__ __launch_bounds__(kThreads) void qk_norm_kernel(QkNormArgs a) {
   for (int n = blockIdx.x * kTokensPerPass + (threadIdx.x >> 4); n < a.L; n += gridDim.x * kTokensPerPass) {
     const bool rot = ROPE && n < rp.n_rot;
     float cs[4] = {1.f, 1.f, 1.f, 1.f}, sn[4] = {0.f, 0.f, 0.f, 0.f};
+    float hcs[8], hsn[8];  // half split: angle of each channel's pair
+#pragma unroll
+    for (int e = 0; e < 8; ++e) { hcs[e] = 1.f; hsn[e] = 0.f; }
     if (rot) {
       const int t = n / (rp.gh * rp.gw);
       const int r = n - t * rp.gh * rp.gw;
       const int h = r / rp.gw;
       const int w = r - h * rp.gw;
+      if (HALF) {
 #pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        const int pos = slot[p].axis == 0 ? t : (slot[p].axis == 1 ? h : w);
-        sincosf((float)pos * omega[p], &sn[p], &cs[p]);
+        for (int e = 0; e < 8; ++e) {
+          const int pos = hax[e] == 0 ? t : (hax[e] == 1 ? h : w);
+          sincosf((float)pos * homega[e], &hsn[e], &hcs[e]);
+        }
+      } else {
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          const int pos = slot[p].axis == 0 ? t : (slot[p].axis == 1 ? h : w);
+          sincosf((float)pos * omega[p], &sn[p], &cs[p]);
+        }
       }
     }
+    float* const row = rowbuf + (HALF ? (threadIdx.x >> 4) * 128 : 0);
     // one row: normalise, scale, rotate and store the 16-byte chunk v
     auto put = [&](uint4 v, size_t off) {
         const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
@@ -95,11 +130,33 @@ __global__ __launch_bounds__(kThreads) void qk_norm_kernel(QkNormArgs a) {
         }
         const float r = rsqrtf(fmaf(row16_sum(ss), inv_d, a.eps));
         uint32_t o[4];
+        if (HALF) {
+          float yv[8], zv[8];
 #pragma unroll
-        for (int p = 0; p < 4; ++p) {
-          const float y0 = xf[2 * p] * r * g[2 * p];
-          const float y1 = xf[2 * p + 1] * r * g[2 * p + 1];
-          o[p] = rot ? pack_bf16x2(fmaf(y0, cs[p], -y1 * sn[p]), fmaf(y0, sn[p], y1 * cs[p])) : pack_bf16x2(y0, y1);
+          for (int e = 0; e < 8; ++e) yv[e] = xf[e] * r * g[e];
+          if (rot) {
+            // the row's normalised values through LDS: written and read by the
+            // 16 lanes of this row (one wave, in order)
+            *reinterpret_cast<float4*>(row + 8 * c) = make_float4(yv[0], yv[1], yv[2], yv[3]);
+            *reinterpret_cast<float4*>(row + 8 * c + 4) = make_float4(yv[4], yv[5], yv[6], yv[7]);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const float yp = row[hpart[e]];
+              zv[e] = hfirst[e] ? fmaf(yv[e], hcs[e], -yp * hsn[e]) : fmaf(yp, hsn[e], yv[e] * hcs[e]);
+            }
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) zv[e] = yv[e];
+          }
+#pragma unroll
+          for (int p = 0; p < 4; ++p) o[p] = pack_bf16x2(zv[2 * p], zv[2 * p + 1]);
+        } else {
+#pragma unroll
+          for (int p = 0; p < 4; ++p) {
+            const float y0 = xf[2 * p] * r * g[2 * p];
+            const float y1 = xf[2 * p + 1] * r * g[2 * p + 1];
+            o[p] = rot ? pack_bf16x2(fmaf(y0, cs[p], -y1 * sn[p]), fmaf(y0, sn[p], y1 * cs[p])) : pack_bf16x2(y0, y1);
+          }
         }
         *reinterpret_cast<uint4*>(a.y + off) = make_uint4(o[0], o[1], o[2], o[3]);
     };
@@ -129,8 +186,9 @@ hipError_t launch_qk_norm(const uint16_t* x, uint16_t* y, const float* gain, flo
   int groups = (L + kTokensPerPass - 1) / kTokensPerPass;
   int grid = groups < 1024 ? groups : 1024;  // 4 workgroups per CU
   if (grid < 1) grid = 1;
-  return rp.enabled ? launch_kernel(qk_norm_kernel<true>, (unsigned)grid, (unsigned)kThreads, stream, a)
-                    : launch_kernel(qk_norm_kernel<false>, (unsigned)grid, (unsigned)kThreads, stream, a);
+  if (!rp.enabled) return launch_kernel(qk_norm_kernel<false, false>, (unsigned)grid, (unsigned)kThreads, stream, a);
+  return rp.pair_mode ? launch_kernel(qk_norm_kernel<true, true>, (unsigned)grid, (unsigned)kThreads, stream, a)
+                      : launch_kernel(qk_norm_kernel<true, false>, (unsigned)grid, (unsigned)kThreads, stream, a);
 }
 
 }  // namespace vidax

@@ -241,7 +241,6 @@ vidax_status vidax_qk_norm_rope(const void* x, void* y, const float* gain, float
     r.keys_prerotated = 0;  // attention-only field
     const vidax_status st = make_rope(&r, L, d, &rp);
     if (st != VIDAX_OK) return st;
-    if (rp.pair_mode != 0) return VIDAX_ERR_UNSUPPORTED;
   }
   if (B == 0 || L == 0 || H == 0) return VIDAX_OK;
   const hipError_t e = vidax::launch_qk_norm((const uint16_t*)x, (uint16_t*)y, gain, eps, B, L, H, rp, stream);

@@ -151,7 +151,8 @@ def _head_scaled(seed, shape, exps):
 
 
 @pytest.mark.parametrize("rotate,with_gain,inplace", [(False, False, False), (False, True, False),
-                                                     (True, True, False), (True, False, True)])
+                                                     (True, True, False), (True, False, True),
+                                                     ("half", True, False), ("half", False, True)])
 @pytest.mark.parametrize("heads", [3, 6])  # head rows are handled four at a time, then one by one
 def test_qk_norm_rope_matches_oracle(rotate, with_gain, inplace, heads):
     import torch
@@ -163,11 +164,12 @@ def test_qk_norm_rope_matches_oracle(rotate, with_gain, inplace, heads):
     log(f"case qk_norm_rope rotate={rotate} gain={with_gain} inplace={inplace} heads={heads}")
     xd = to_dev(x)
     gd = torch.from_numpy(g).cuda() if with_gain else None
-    r = vx.Rope(grid=grid, dims=(44, 42, 42), theta=10000.0) if rotate else None
+    mode = 1 if rotate == "half" else 0  # "half": half-split pairs
+    r = vx.Rope(grid=grid, dims=(44, 42, 42), theta=10000.0, pair_mode=mode) if rotate else None
     y = vx.qk_norm_rope(xd, r, gain=gd, eps=eps, out=xd if inplace else None)
     torch.cuda.synchronize()
     got = oracle.bf16_bits_to_f64(to_bits(y))
-    spec = oracle.RopeSpec(grid=grid) if rotate else None
+    spec = oracle.RopeSpec(grid=grid, pair_mode=mode) if rotate else None
     xf = oracle.bf16_bits_to_f64(x)
     gain = g.astype(np.float64) if with_gain else None
     ref = oracle.qk_norm_ref(xf, gain=gain, eps=eps, rope=spec)
@@ -286,6 +288,32 @@ def test_prerotated_keys(w):
     ro, rl = _oracle_full(w, q, k, v, lv)
     assert_parity(to_bits(o), ro, f"{w.name} prerotated")
     assert_lse(l.cpu().numpy(), rl, f"{w.name} prerotated")
+
+
+@pytest.mark.parametrize("w", [inputs.WORKLOADS["tiny"], RAGGED[0], RAGGED[5]], ids=lambda w: w.name)
+def test_half_split_pairs_prerotated_keys(w):
+    """Half-split pairs (channel o_a + j with o_a + j + d_a/2): k rotated by
+    vidax_rope3d, q inside the attention kernel (each channel's partner from
+    the staged query row), against the oracle with the same convention."""
+    import dataclasses
+
+    import torch
+
+    q, k, v, lv = inputs.make_qkv(w)
+    log(f"case half-split pairs {w.name}")
+    r = dataclasses.replace(rope_of(w), pair_mode=1)
+    krot = vx.rope3d(to_dev(k), r)
+    o, l = vx.attn_fwd(to_dev(q), krot, to_dev(v), scale=w.scale, kv_valid_len=lengths_dev(lv),
+                       rope=dataclasses.replace(r, keys_prerotated=True), return_lse=True)
+    torch.cuda.synchronize()
+    dec = oracle.bf16_bits_to_f64
+    spec = dataclasses.replace(spec_of(w), pair_mode=1)
+    ro, rl = oracle.attn_ref(dec(q), dec(k), dec(v), w.scale, kv_valid_len=lv, rope=spec, workers=8)
+    assert_parity(to_bits(o), ro, f"{w.name} half split")
+    assert_lse(l.cpu().numpy(), rl, f"{w.name} half split")
+    # the interleaved result differs (the convention is really applied)
+    ri, _ = _oracle_full(w, q, k, v, lv)
+    assert np.abs(ri - ro).max() > 1e-2
 
 
 def test_zero_and_single_valid_keys():

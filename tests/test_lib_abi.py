@@ -83,7 +83,8 @@ def test_attn_rejects_invalid_arguments(fn):
     del good
 
 
-def test_half_split_only_on_naive_and_rope3d():
+def test_half_split_attention_needs_prerotated_keys():
+    # the fused key rotation pairs interleaved channels only
     r = vx.Rope((1, 8, 8), (44, 42, 42), pair_mode=1).desc()
     assert _attn("vidax_attn_fwd", rope=r) == 2
 
@@ -127,7 +128,7 @@ def test_qk_norm_rope_rejects_invalid_arguments():
     assert call(L=63) == 1                           # 64 rotated tokens > L
     assert call(y=P + 256) == 1                      # partial overlap (in place is x == y)
     assert call(gain=2 * P + 512) == 1               # gain overlaps the output
-    assert call(rope=vx.Rope((2, 4, 8), (44, 42, 42), pair_mode=1).desc()) == 2  # half split: unsupported
+    assert call(rope=vx.Rope((2, 4, 8), (44, 42, 42), pair_mode=2).desc()) == 1  # no such pair convention
     assert call(rope=vx.Rope((2, 4, 8), (40, 42, 42)).desc()) == 1               # widths do not sum to d
 
 
