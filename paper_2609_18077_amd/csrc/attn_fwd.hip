@@ -177,7 +177,8 @@ constexpr int kAttnShortKeys = 1024;
 
 // ROPE: rotate the queries (and build the table); ROPE_K: also rotate the keys
 // while staging them (false when the caller passes pre-rotated keys).
-template <bool ROPE, bool ROPE_K>
+// HALF: half-split pairs (queries only; ROPE_K is then false).
+template <bool ROPE, bool ROPE_K, bool HALF = false>
 __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   // Two K and two V buffers, each its own LDS object so that the compiler can
   // tell the direct copies into one buffer from the operand reads of another
@@ -255,29 +256,39 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
 
   // ---- Q: lane holds query qrow, d-chunks 2s + hi (s = 0..7) as MFMA B operands
   bf16x8 qreg[8];
-  // Half-split pairs (keys then come rotated by vidax_rope3d): channel ch of
-  // the block of axis a (offset o_a, width d_a) pairs with ch +- d_a / 2,
-  // which another lane holds; it is read from the query row still in the
-  // staging area.  Returns the rotated, scaled channel ch of the lane's query.
-  auto half_split_q = [&](int ch, float x, uint32_t qpos, float qm) __attribute__((always_inline)) {
+  // Half-split pairs (keys then come rotated by vidax_rope3d): pair j of the
+  // block of axis a (offset o_a, width d_a) is channels o_a + j and
+  // o_a + j + d_a / 2, which different lanes read out.  So the staged query
+  // row is rotated and scaled in place first, the two lanes of a row taking
+  // 32 pairs each (one rounding, as in the interleaved path), and make_q then
+  // takes the values as they are.
+  auto rotate_staged_half_split = [&]() __attribute__((always_inline)) {
     const RopeParams& r = a.rp;
-    int o, hl, pb;  // block offset, half width, pairs of the blocks before it
-    if (ch < r.dt) { o = 0; hl = r.dt >> 1; pb = 0; }
-    else if (ch < r.dt + r.dh) { o = r.dt; hl = r.dh >> 1; pb = r.dt >> 1; }
-    else { o = r.dt + r.dh; hl = r.dw >> 1; pb = (r.dt >> 1) + (r.dh >> 1); }
-    const bool first = ch - o < hl;
-    const int j = first ? ch - o : ch - o - hl;
-    const int pc = first ? ch + hl : ch - hl;
-    const float xp = __uint_as_float((uint32_t)stage[l32 * D + stage_slot(pc >> 3, l32) * 8 + (pc & 7)] << 16);
-    const float2 cs = table_entry(tab, pair_idx(a, pb + j), qpos);
-    return (first ? fmaf(x, cs.x, -xp * cs.y) : fmaf(xp, cs.y, x * cs.x)) * qm;
+    const uint32_t qpos = packed_pos(a, qlive ? qrow : r.n_rot);
+    const float qm = a.qmul;
+    uint16_t* const row = stage + l32 * D;
+    const int ht = r.dt >> 1, hh = r.dh >> 1;
+#pragma unroll 1
+    for (int pi = 32 * hi; pi < 32 * hi + 32; ++pi) {
+      int o, hl, j;
+      if (pi < ht) { o = 0; hl = ht; j = pi; }
+      else if (pi < ht + hh) { o = r.dt; hl = hh; j = pi - ht; }
+      else { o = r.dt + r.dh; hl = r.dw >> 1; j = pi - ht - hh; }
+      const int c0 = o + j, c1 = c0 + hl;
+      uint16_t* const p0 = row + stage_slot(c0 >> 3, l32) * 8 + (c0 & 7);
+      uint16_t* const p1 = row + stage_slot(c1 >> 3, l32) * 8 + (c1 & 7);
+      const float x0 = __uint_as_float((uint32_t)*p0 << 16), x1 = __uint_as_float((uint32_t)*p1 << 16);
+      const float2 cs = table_entry(tab, pair_idx(a, pi), qpos);
+      const uint32_t y = pack_bf16x2(fmaf(x0, cs.x, -x1 * cs.y) * qm, fmaf(x0, cs.y, x1 * cs.x) * qm);
+      *p0 = (uint16_t)(y & 0xffffu);
+      *p1 = (uint16_t)(y >> 16);
+    }
   };
   auto make_q = [&](const uint4 raw[8]) __attribute__((always_inline)) {
     const uint32_t qpos = ROPE ? packed_pos(a, qlive ? qrow : a.rp.n_rot) : 0u;
     const float qm = a.qmul;
     const uint32_t sgn = a.qsign < 0.f ? 0x80008000u : 0u;
     const uint32_t keep = a.qsign == 0.f ? 0u : 0xffffffffu;
-    const bool half = ROPE && a.rp.pair_mode != 0;  // uniform
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       const int c = 2 * s + hi;
@@ -285,10 +296,8 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
 #pragma unroll
       for (int p = 0; p < 4; ++p) {
         if (ROPE) {  // rotated and scaled in fp32, rounded once
-          const float x0 = bf16lo_to_f32(wq[p]), x1 = bf16hi_to_f32(wq[p]);
-          if (half) {
-            wq[p] = pack_bf16x2(half_split_q(8 * c + 2 * p, x0, qpos, qm), half_split_q(8 * c + 2 * p + 1, x1, qpos, qm));
-          } else {
+          if (!HALF) {  // (half-split rows were rotated in the staging area)
+            const float x0 = bf16lo_to_f32(wq[p]), x1 = bf16hi_to_f32(wq[p]);
             const float2 cs = table_entry(tab, pair_idx(a, 4 * c + p), qpos);
             wq[p] = pack_bf16x2(fmaf(x0, cs.x, -x1 * cs.y) * qm, fmaf(x0, cs.y, x1 * cs.x) * qm);
           }
@@ -672,6 +681,7 @@ __global__ __launch_bounds__(NT) void attn_fwd_kernel(AttnArgs a) {
   }
   __builtin_amdgcn_s_waitcnt(0);  // this wave's query rows have landed
   {
+    if (HALF) rotate_staged_half_split();
     uint4 raw[8];
     read_q(raw);
     make_q(raw);
@@ -742,6 +752,8 @@ hipError_t launch_attn_fwd(const uint16_t* q, const uint16_t* k, const uint16_t*
     return launch_xattn_fwd(q, k, v, o, lse, B, H, Lq, Lk, scale, kv_valid_len, cus, stream);
   if (rp.enabled && !rp.keys_prerotated)
     return launch_kernel(attn_fwd_kernel<true, true>, (unsigned)nwg, (unsigned)NT, stream, a);
+  if (rp.enabled && rp.pair_mode != 0)
+    return launch_kernel(attn_fwd_kernel<true, false, true>, (unsigned)nwg, (unsigned)NT, stream, a);
   if (rp.enabled) return launch_kernel(attn_fwd_kernel<true, false>, (unsigned)nwg, (unsigned)NT, stream, a);
   return launch_kernel(attn_fwd_kernel<false, false>, (unsigned)nwg, (unsigned)NT, stream, a);
 }
