@@ -271,9 +271,8 @@ vidax_status vidax_na3d_fwd(const void* q, const void* k, const void* v, void* o
  *
  * where rms_norm acts on each (token, head) over its d channels with eps, as
  * in vidax_qk_norm_rope; gains fp32 [d] (shared by the heads) or NULL (unit);
- * rope as vidax_rope3d (token n of each sequence of L, interleaved pairs
- * only: VIDAX_ERR_UNSUPPORTED for pair_mode 1, whose models project without
- * rope and then call vidax_qk_norm_rope), or NULL for none.  q, k, v: bf16 [B, L, H, d] outputs, rounded once.
+ * rope as vidax_rope3d (token n of each sequence of L, either pair_mode), or
+ * NULL for none.  q, k, v: bf16 [B, L, H, d] outputs, rounded once.
  * fp32 accumulation.  All pointers 16-byte aligned; outputs must not overlap
  * each other or an input.  Requires d == 128 and C a multiple of 64
  * (VIDAX_ERR_UNSUPPORTED otherwise); eps >= 0 finite.

@@ -79,6 +79,8 @@ __device__ __forceinline__ float half_swap_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// HALF: half-split rotary pairs (channel o_a + j with o_a + j + d_a / 2)
+template <bool HALF>
 __global__ __launch_bounds__(NT) void qkv_proj_kernel(QkvArgs a) {
   // tile layout: row r at element r * kPitch, 16-byte chunk c of the stage's
   // 64 input channels at + 8 c
@@ -235,7 +237,56 @@ __global__ __launch_bounds__(NT) void qkv_proj_kernel(QkvArgs a) {
           acc[cb][tb][4 * g + 3] *= gg.w;
         }
       const int n = m % a.L;  // position in the sequence
-      if (rp.enabled && n < rp.n_rot) {
+      if (HALF) {
+        // A channel's partner lies d_a / 2 further in its axis block, in
+        // another register or the other lane half: the token's values go
+        // through wave-private fp32 rows in X1 (free now), an eighth of the
+        // wave's tokens at a time: the two lanes of a token write their
+        // halves to row x, rotate their channels from row x into row y in a
+        // plain loop, and read row y back (one wave, in order: no barrier).
+        float* const xrow = reinterpret_cast<float*>(X1) + (wave * 8 + (l32 & 3)) * D;
+        float* const yrow = xrow + 4 * D;
+        const bool rot = n < rp.n_rot;
+        const int t = n / (rp.gh * rp.gw);
+        const int rr = n - t * rp.gh * rp.gw;
+        const int hh = rr / rp.gw;
+        const int ww = rr - hh * rp.gw;
+        const int ht = rp.dt >> 1, hd = rp.dh >> 1;
+        for (int pass = 0; pass < 8; ++pass) {
+          if ((l32 >> 2) != pass || !rot) continue;
+#pragma unroll
+          for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+              *reinterpret_cast<float4*>(xrow + 32 * cb + 8 * g + 4 * hi) =
+                  make_float4(acc[cb][tb][4 * g], acc[cb][tb][4 * g + 1], acc[cb][tb][4 * g + 2], acc[cb][tb][4 * g + 3]);
+#pragma unroll 1
+          for (int k = 0; k < 64; ++k) {
+            const int ch = 32 * (k >> 4) + 8 * ((k >> 2) & 3) + 4 * hi + (k & 3);
+            int o, hl, pb;
+            if (ch < rp.dt) { o = 0; hl = ht; pb = 0; }
+            else if (ch < rp.dt + rp.dh) { o = rp.dt; hl = hd; pb = ht; }
+            else { o = rp.dt + rp.dh; hl = rp.dw >> 1; pb = ht + hd; }
+            const bool first = ch - o < hl;
+            const int j = first ? ch - o : ch - o - hl;
+            const PairSlot sl = pair_slot(rp, pb + j);
+            const int pos = sl.axis == 0 ? t : (sl.axis == 1 ? hh : ww);
+            const float2 e = tab[sl.base + pos * sl.stride];
+            const float x = xrow[ch], xp = xrow[first ? ch + hl : ch - hl];
+            yrow[ch] = first ? fmaf(x, e.x, -xp * e.y) : fmaf(xp, e.y, x * e.x);
+          }
+#pragma unroll
+          for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              const float4 y = *reinterpret_cast<const float4*>(yrow + 32 * cb + 8 * g + 4 * hi);
+              acc[cb][tb][4 * g] = y.x;
+              acc[cb][tb][4 * g + 1] = y.y;
+              acc[cb][tb][4 * g + 2] = y.z;
+              acc[cb][tb][4 * g + 3] = y.w;
+            }
+        }
+      } else if (rp.enabled && n < rp.n_rot) {
         const int t = n / (rp.gh * rp.gw);
         const int rr = n - t * rp.gh * rp.gw;
         const int hh = rr / rp.gw;
@@ -290,7 +341,8 @@ hipError_t launch_qkv_proj(const uint16_t* x, const uint16_t* w, const float* bi
   a.ntm = (a.M + BMT - 1) / BMT;
   a.nwg = a.ntn * a.ntm;
   a.rp = rp;
-  return launch_kernel(qkv_proj_kernel, (unsigned)a.nwg, (unsigned)NT, stream, a);
+  return rp.enabled && rp.pair_mode ? launch_kernel(qkv_proj_kernel<true>, (unsigned)a.nwg, (unsigned)NT, stream, a)
+                                     : launch_kernel(qkv_proj_kernel<false>, (unsigned)a.nwg, (unsigned)NT, stream, a);
 }
 
 }  // namespace vidax

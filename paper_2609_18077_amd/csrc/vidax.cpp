@@ -323,7 +323,6 @@ vidax_status vidax_qkv_proj(const void* x, const void* w, const float* bias, con
     r.keys_prerotated = 0;  // attention-only field
     const vidax_status st = make_rope(&r, L, d, &rp);
     if (st != VIDAX_OK) return st;
-    if (rp.pair_mode != 0) return VIDAX_ERR_UNSUPPORTED;
   }
   if (no == 0) return VIDAX_OK;
   const uint64_t ob = (uint64_t)no * 2;

@@ -39,20 +39,20 @@ def _dev(a, dtype):
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
 
 
-def _spec(w):
-    return None if w.grid is None else oracle.RopeSpec(grid=w.grid, dims=w.dims, theta=w.theta)
+def _spec(w, mode=0):
+    return None if w.grid is None else oracle.RopeSpec(grid=w.grid, dims=w.dims, theta=w.theta, pair_mode=mode)
 
 
-def _rope(w):
-    return None if w.grid is None else vx.Rope(w.grid, w.dims, w.theta)
+def _rope(w, mode=0):
+    return None if w.grid is None else vx.Rope(w.grid, w.dims, w.theta, pair_mode=mode)
 
 
-def _run(w):
+def _run(w, mode=0):
     import torch
 
     x, wt, bias, gq, gk = inputs.make_proj_inputs(w)
     q, k, v = vx.qkv_proj(_dev(x, "bf16"), _dev(wt, "bf16"), w.B, w.L, w.H, bias=_dev(bias, "f32"),
-                          gain_q=_dev(gq, "f32"), gain_k=_dev(gk, "f32"), eps=w.eps, rope=_rope(w))
+                          gain_q=_dev(gq, "f32"), gain_k=_dev(gk, "f32"), eps=w.eps, rope=_rope(w, mode))
     torch.cuda.synchronize()
     return (x, wt, bias, gq, gk), (to_bits(q), to_bits(k), to_bits(v))
 
@@ -137,6 +137,19 @@ def test_qkv_proj_matches_oracle(w):
     sb = _sum_bounds(w, x, wt, bias, gq, gk)
     for name, g, r, e in zip("qkv", got, ref, sb):
         _check(g, r, name, e, _spec(w) if name != "v" else None)
+
+
+@pytest.mark.parametrize("w", [PROJ[0], PROJ[1], PROJ[3]], ids=lambda w: w.name)
+def test_qkv_proj_half_split_pairs(w):
+    """Half-split rotary pairs (channel o_a + j with o_a + j + d_a/2) in the
+    epilogue, against the oracle in that convention."""
+    log(f"case qkv half split {w.name} B{w.B} L{w.L} H{w.H} C{w.C} grid={w.grid}")
+    (x, wt, bias, gq, gk), got = _run(w, mode=1)
+    dec = oracle.bf16_bits_to_f64
+    ref = oracle.qkv_proj_ref(dec(x), dec(wt), bias, w.B, w.L, w.H, w.d, gq, gk, w.eps, _spec(w, 1))
+    sb = _sum_bounds(w, x, wt, bias, gq, gk)
+    for name, g, r, e in zip("qkv", got, ref, sb):
+        _check(g, r, name, e, _spec(w, 1) if name != "v" else None)
 
 
 def test_qkv_proj_full_size_sampled():

@@ -264,8 +264,8 @@ def test_qkv_proj_rejects_invalid_arguments():
     assert call(q=P) == INV                 # output aliases x
     assert call(v=2 * P + 512) == INV       # output inside w
     assert call(k=6 * P + 1024) == INV      # outputs overlap
-    bad = vx.Rope((2, 4, 8), (44, 42, 42), pair_mode=1).desc()
-    assert call(rope=bad) == UNS            # half-split pairs
+    bad = vx.Rope((2, 4, 8), (44, 42, 42), pair_mode=2).desc()
+    assert call(rope=bad) == INV            # no such pair convention
     assert call(rope=good, L=63) == INV     # more rotated tokens than L
     assert call(B=0, x=0, w=0, q=0, k=0, v=0) == 0  # empty
     assert call(bias=0, gq=0, gk=0, C=0, L=0) == 0
