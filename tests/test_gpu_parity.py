@@ -497,7 +497,27 @@ def _random_persistent(n=6, seed=2027):
     return cases
 
 
-@pytest.mark.parametrize("w", PERSISTENT + _random_persistent(), ids=lambda w: w.name)
+def _random_persistent_many_batches(n=6, seed=2031):
+    """More seeded random short-key shapes: 3 to 6 batches with lengths drawn
+    from [1, Lk], Lk up to 1024, so consecutive batches have different tile
+    counts (1 to 16) and the kept K/V buffers meet head changes between them
+    often; ragged Lq."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        B = int(rng.integers(3, 7))
+        H = int(rng.integers(2, 9))
+        Lk = int(rng.choice([300, 640, 1000, 1024]))
+        need = 1024 // (B * H) + 2
+        Lq = int(rng.integers(need * 256 - 255, need * 256 + 2000))
+        lens = [int(x) for x in rng.integers(1, Lk + 1, B)]
+        cases.append(inputs.custom(f"prand_many{i}", B=B, H=H, Lq=Lq, Lk=Lk, seed=320 + i,
+                                   kv_valid=("fixed", lens)))
+    return cases
+
+
+@pytest.mark.parametrize("w", PERSISTENT + _random_persistent() + _random_persistent_many_batches(),
+                         ids=lambda w: w.name)
 def test_persistent_short_keys_sampled(w):
     import torch
 
